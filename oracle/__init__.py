@@ -1,0 +1,148 @@
+"""CPU oracle for the tree-verification step (TEST INFRASTRUCTURE ONLY).
+
+Only `tests/`, `__graft_entry__.smoke()` and the benchmark's `cpu_baseline`
+leg may import this package. The GPU library never links, loads or calls it,
+and it shares no code with the GPU library.
+
+The arithmetic lives in `oracle.c` (plain C, fp64, OpenMP across independent
+items); this module only compiles it with gcc and marshals numpy arrays.
+Each wrapper cites the passage of the paper the C function follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc (fp64, no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+               "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        p = ctypes.c_void_p
+        i = ctypes.c_int
+        lib.oracle_tree_attention.argtypes = [p] * 8 + [i] * 8 + [ctypes.c_double, p, p]
+        lib.oracle_tree_attention.restype = i
+        lib.oracle_argmax.argtypes = [p, ctypes.c_long, ctypes.c_long, p]
+        lib.oracle_argmax.restype = None
+        lib.oracle_accept.argtypes = [p, p, p, i, i, p, p, p]
+        lib.oracle_accept.restype = i
+        lib.oracle_kv_compact.argtypes = [p] * 8 + [i] * 7
+        lib.oracle_kv_compact.restype = i
+        lib.oracle_num_threads.argtypes = []
+        lib.oracle_num_threads.restype = i
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"], "oracle inputs must be C-contiguous"
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def tree_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent,
+                   scale: float = 0.0):
+    """Tree-masked attention (§2.1 tree-shaped verification mask; §8 SpecInfer
+    masking; §1 attention over all cached keys). Inputs are bf16 bit arrays in
+    the layouts of `paper_2602_21224_amd.workloads`. Returns (out, lse) as fp64
+    arrays [B, N, Hq, D] and [B, N, Hq]."""
+    q = _c(q, np.uint16)
+    k_tree = _c(k_tree, np.uint16)
+    v_tree = _c(v_tree, np.uint16)
+    k_cache = _c(k_cache, np.uint16)
+    v_cache = _c(v_cache, np.uint16)
+    page_table = _c(page_table, np.int32)
+    kv_len = _c(kv_len, np.int32)
+    parent = _c(parent, np.int32)
+    B, N, Hq, D = q.shape
+    Hkv = k_tree.shape[2]
+    num_pages, P = k_cache.shape[0], k_cache.shape[1]
+    max_pages = page_table.shape[1]
+    out = np.zeros((B, N, Hq, D), dtype=np.float64)
+    lse = np.zeros((B, N, Hq), dtype=np.float64)
+    rc = _load().oracle_tree_attention(
+        _ptr(q), _ptr(k_tree), _ptr(v_tree), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
+        _ptr(kv_len), _ptr(parent), B, N, Hq, Hkv, D, P, max_pages, num_pages,
+        float(scale), _ptr(out), _ptr(lse))
+    if rc != 0:
+        raise ValueError("oracle_tree_attention rejected its arguments")
+    return out, lse
+
+
+def argmax(logits):
+    """Per-row greedy argmax (§7.1 evaluates at temperature 0): lowest index of
+    the maximum, -0 == +0, first NaN wins. logits [..., V] fp32 -> int32 [...]."""
+    logits = _c(logits, np.float32)
+    V = logits.shape[-1]
+    rows = logits.size // V if V else 0
+    out = np.zeros(logits.shape[:-1], dtype=np.int32)
+    _load().oracle_argmax(_ptr(logits), rows, V, _ptr(out))
+    return out
+
+
+def accept(draft, parent, amax):
+    """Greedy longest accepted path and bonus token (§5.3; Alg. 2's
+    ground-truth token). Returns (accept_len [B], accept_idx [B, N], bonus [B])."""
+    draft = _c(draft, np.int32)
+    parent = _c(parent, np.int32)
+    amax = _c(amax, np.int32)
+    B, N = parent.shape
+    alen = np.zeros(B, dtype=np.int32)
+    aidx = np.zeros((B, N), dtype=np.int32)
+    bonus = np.zeros(B, dtype=np.int32)
+    rc = _load().oracle_accept(_ptr(draft), _ptr(parent), _ptr(amax), B, N,
+                               _ptr(alen), _ptr(aidx), _ptr(bonus))
+    if rc != 0:
+        raise ValueError("oracle_accept: parent[i] must lie in [-1, i-1]")
+    return alen, aidx, bonus
+
+
+def kv_compact(k_tree, v_tree, k_cache, v_cache, page_table, kv_len, accept_idx, accept_len):
+    """Copy the accepted path's K/V rows to cache positions kv_len .. kv_len +
+    accept_len - 1 (§1 KV cache of committed tokens). Works on copies; returns
+    the new (k_cache, v_cache)."""
+    k_tree = _c(k_tree, np.uint16)
+    v_tree = _c(v_tree, np.uint16)
+    kc = np.array(k_cache, dtype=np.uint16, order="C", copy=True)
+    vc = np.array(v_cache, dtype=np.uint16, order="C", copy=True)
+    page_table = _c(page_table, np.int32)
+    kv_len = _c(kv_len, np.int32)
+    accept_idx = _c(accept_idx, np.int32)
+    accept_len = _c(accept_len, np.int32)
+    B, N, Hkv, D = k_tree.shape
+    num_pages, P = kc.shape[0], kc.shape[1]
+    rc = _load().oracle_kv_compact(_ptr(k_tree), _ptr(v_tree), _ptr(kc), _ptr(vc),
+                                   _ptr(page_table), _ptr(kv_len), _ptr(accept_idx),
+                                   _ptr(accept_len), B, N, Hkv, D, P, page_table.shape[1],
+                                   num_pages)
+    if rc != 0:
+        raise ValueError("oracle_kv_compact: destination outside the page table or pool")
+    return kc, vc

@@ -1,0 +1,340 @@
+"""Seeded synthetic inputs for the target-model tree-verification step.
+
+This module only *draws* inputs: draft trees (parent links and token ids), a
+paged bf16 KV cache, bf16 queries and tree keys/values, and fp32 vocabulary
+logits. It performs none of the verification arithmetic (no attention, no
+argmax, no acceptance, no compaction), so both the GPU path and the CPU oracle
+can consume the same bytes without sharing any of the method's code.
+
+Shapes follow the draft-tree verification setting of the paper: a tree of
+draft tokens whose nodes carry a token and a parent (Alg. 1's Node structure,
+§5.2), rooted at the last verified token (§5.2), verified in one target pass
+over a paged KV cache (§7.1 uses Paged Attention). The five named presets are
+Llama-shaped stand-ins for the paper's serving workload (§7.1, which uses an
+unnamed SGLang benchmark set); no dataset item is reproduced.
+
+Layouts (all C-contiguous):
+  q        uint16 (bf16 bits) [B, N, Hq, D]
+  k_tree   uint16             [B, N, Hkv, D]
+  v_tree   uint16             [B, N, Hkv, D]
+  k_cache  uint16             [num_pages, P, Hkv, D]
+  v_cache  uint16             [num_pages, P, Hkv, D]
+  page_table int32            [B, max_pages]   (-1 beyond what a sequence owns)
+  kv_len   int32              [B]
+  parent   int32              [B, N]           (parent[b, i] in [-1, i-1])
+  draft    int32              [B, N]
+  logits   float32            [B, N, V]
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+PAGE_SIZE = 16
+BF16_NAN = np.uint16(0x7FC0)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round finite float32 values to bf16 (round-to-nearest-even), return raw bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounding = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + rounding) >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(h: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bits to float32 (used by tests for fixtures)."""
+    return (np.asarray(h, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+@dataclass
+class Workload:
+    name: str
+    B: int
+    N: int
+    Hq: int
+    Hkv: int
+    D: int
+    P: int
+    V: int
+    q: np.ndarray
+    k_tree: np.ndarray
+    v_tree: np.ndarray
+    k_cache: np.ndarray
+    v_cache: np.ndarray
+    page_table: np.ndarray
+    kv_len: np.ndarray
+    parent: np.ndarray
+    draft: np.ndarray
+    logits: np.ndarray | None
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def max_pages(self) -> int:
+        return int(self.page_table.shape[1])
+
+    @property
+    def num_pages(self) -> int:
+        return int(self.k_cache.shape[0])
+
+    @property
+    def max_kv_len(self) -> int:
+        return int(self.kv_len.max()) if self.B else 0
+
+
+# --------------------------------------------------------------------------
+# tree shapes (parent arrays in topological order: parent[i] < i)
+# --------------------------------------------------------------------------
+
+def tree_uniform_forest(rng: np.random.Generator, n: int) -> np.ndarray:
+    """parent[i] uniform over {-1, 0, ..., i-1}; several roots are possible."""
+    parent = np.empty(n, dtype=np.int32)
+    for i in range(n):
+        parent[i] = rng.integers(-1, i) if i > 0 else -1
+    return parent
+
+
+def tree_random_depth_capped(rng: np.random.Generator, n: int, depth_lt: int,
+                             root_children: int = 0) -> np.ndarray:
+    """Node 0 is the root; optionally nodes 1..root_children hang off it; every
+    later node picks a parent uniformly among earlier nodes of depth < depth_lt."""
+    parent = np.full(n, -1, dtype=np.int32)
+    depth = np.zeros(n, dtype=np.int64)
+    for i in range(1, n):
+        if i <= root_children:
+            p = 0
+        else:
+            cand = np.nonzero(depth[:i] < depth_lt)[0]
+            p = int(cand[rng.integers(0, len(cand))])
+        parent[i] = p
+        depth[i] = depth[p] + 1
+    return parent
+
+
+def tree_topk_expansion(rng: np.random.Generator, branching, keep: int):
+    """Expand a root level by level with the given children-per-node counts;
+    child probabilities are the top-b entries of a sorted Dirichlet(1 x 8)
+    draw; keep the `keep` nodes of highest joint probability (ties to the
+    lower BFS index) and relabel them in BFS order. Returns the parent array.
+    This mirrors how a draft tree is built and pruned to a verification budget
+    (Alg. 1 and the budget pruning of §5.2) only to shape the synthetic input."""
+    par = [-1]
+    joint = [1.0]
+    frontier = [0]
+    for b in branching:
+        nxt = []
+        for node in frontier:
+            probs = np.sort(rng.dirichlet(np.ones(8)))[::-1][:b]
+            for pr in probs:
+                par.append(node)
+                joint.append(joint[node] * float(pr))
+                nxt.append(len(par) - 1)
+        frontier = nxt
+    joint_a = np.asarray(joint)
+    order = sorted(range(len(par)), key=lambda i: (-joint_a[i], i))
+    kept = sorted(order[:keep])
+    relabel = {old: new for new, old in enumerate(kept)}
+    parent = np.empty(len(kept), dtype=np.int32)
+    for new, old in enumerate(kept):
+        p = par[old]
+        if p >= 0 and p not in relabel:
+            raise AssertionError("pruned tree is not ancestor-closed")
+        parent[new] = -1 if p < 0 else relabel[p]
+    return parent
+
+
+def tree_depths(parent: np.ndarray) -> np.ndarray:
+    d = np.zeros(len(parent), dtype=np.int64)
+    for i, p in enumerate(parent):
+        d[i] = 0 if p < 0 else d[p] + 1
+    return d
+
+
+def tree_chain(n: int) -> np.ndarray:
+    return np.arange(-1, n - 1, dtype=np.int32)
+
+
+def tree_star(n: int) -> np.ndarray:
+    p = np.zeros(n, dtype=np.int32)
+    p[0] = -1
+    return p
+
+
+# --------------------------------------------------------------------------
+# draft tokens and logits
+# --------------------------------------------------------------------------
+
+def draft_tokens(rng: np.random.Generator, parent: np.ndarray, V: int,
+                 distinct_siblings: bool) -> np.ndarray:
+    n = len(parent)
+    tok = rng.integers(0, V, size=n).astype(np.int32)
+    if distinct_siblings:
+        seen: dict[int, set] = {}
+        for i in range(n):
+            s = seen.setdefault(int(parent[i]), set())
+            while int(tok[i]) in s and len(s) < V:
+                tok[i] = rng.integers(0, V)
+            s.add(int(tok[i]))
+    return tok
+
+
+def boost_logits(rng: np.random.Generator, logits_b: np.ndarray, parent: np.ndarray,
+                 draft: np.ndarray, prob: float, amount: float) -> None:
+    """For each node that has children, with probability `prob` add `amount`
+    to that node's logit of one uniformly chosen child's draft token."""
+    n = len(parent)
+    children: dict[int, list] = {}
+    for i in range(n):
+        if parent[i] >= 0:
+            children.setdefault(int(parent[i]), []).append(i)
+    for p in range(n):
+        ch = children.get(p)
+        if not ch:
+            continue
+        if rng.random() < prob:
+            c = ch[int(rng.integers(0, len(ch)))]
+            logits_b[p, draft[c]] += np.float32(amount)
+
+
+# --------------------------------------------------------------------------
+# paged cache
+# --------------------------------------------------------------------------
+
+def paged_layout(rng: np.random.Generator, kv_len: np.ndarray, N: int, P: int):
+    """Give each sequence ceil((L_b + N) / P) pages (room for the accepted
+    path), drawn from one seeded permutation of the pool. Returns
+    (page_table [B, max_pages] with -1 padding, num_pages)."""
+    need = [(int(L) + N + P - 1) // P for L in kv_len]
+    total = int(sum(need))
+    max_pages = max(need) if need else 1
+    perm = rng.permutation(total).astype(np.int32)
+    pt = np.full((len(kv_len), max_pages), -1, dtype=np.int32)
+    off = 0
+    for b, k in enumerate(need):
+        pt[b, :k] = perm[off:off + k]
+        off += k
+    return pt, total
+
+
+def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
+    return f32_to_bf16_bits(rng.standard_normal(size=shape, dtype=np.float32))
+
+
+def poison_cache_tails(k_cache, v_cache, page_table, kv_len, P) -> None:
+    """Fill every cache slot that no sequence's prefix covers with bf16 NaN."""
+    num_pages = k_cache.shape[0]
+    used = np.zeros((num_pages, P), dtype=bool)
+    for b in range(len(kv_len)):
+        L = int(kv_len[b])
+        for t in range(0, L, P):
+            pg = page_table[b, t // P]
+            used[pg, : min(P, L - t)] = True
+    k_cache[~used] = BF16_NAN
+    v_cache[~used] = BF16_NAN
+
+
+def make_workload(name: str, seed: int, *, B: int, N: int, Hq: int, Hkv: int, D: int,
+                  kv_len, parent_fn, V: int, boost_prob: float = 0.0,
+                  boost_amount: float = 3.0, P: int = PAGE_SIZE,
+                  distinct_siblings: bool = True, poison: bool = False,
+                  with_logits: bool = True, forced_path=None) -> Workload:
+    """Draw one workload. `kv_len` is an int, a (lo, hi) inclusive range, or
+    an explicit per-sequence list; `parent_fn(rng)` returns one tree."""
+    ss = np.random.SeedSequence(seed)
+    r_tree, r_len, r_page, r_q, r_kv, r_tree_kv, r_tok, r_logit, r_boost = [
+        np.random.default_rng(s) for s in ss.spawn(9)]
+
+    parent = np.stack([np.asarray(parent_fn(r_tree), dtype=np.int32) for _ in range(B)]) \
+        if B else np.zeros((0, N), np.int32)
+    assert parent.shape == (B, N)
+
+    if isinstance(kv_len, (int, np.integer)):
+        lens = np.full(B, int(kv_len), dtype=np.int32)
+    elif isinstance(kv_len, tuple):
+        lo, hi = kv_len
+        lens = r_len.integers(lo, hi + 1, size=B).astype(np.int32)
+    else:
+        lens = np.asarray(kv_len, dtype=np.int32)
+    assert lens.shape == (B,)
+
+    page_table, num_pages = paged_layout(r_page, lens, N, P)
+    q = _normal_bf16(r_q, (B, N, Hq, D))
+    k_cache = _normal_bf16(r_kv, (num_pages, P, Hkv, D))
+    v_cache = _normal_bf16(r_kv, (num_pages, P, Hkv, D))
+    k_tree = _normal_bf16(r_tree_kv, (B, N, Hkv, D))
+    v_tree = _normal_bf16(r_tree_kv, (B, N, Hkv, D))
+    if poison:
+        poison_cache_tails(k_cache, v_cache, page_table, lens, P)
+
+    draft = np.stack([draft_tokens(r_tok, parent[b], V, distinct_siblings) for b in range(B)]) \
+        if B else np.zeros((0, N), np.int32)
+
+    logits = None
+    if with_logits:
+        logits = r_logit.standard_normal(size=(B, N, V), dtype=np.float32)
+        for b in range(B):
+            if boost_prob > 0.0:
+                boost_logits(r_boost, logits[b], parent[b], draft[b], boost_prob, boost_amount)
+            if forced_path is not None:
+                for c in forced_path(parent[b]):
+                    logits[b, parent[b, c], draft[b, c]] += np.float32(1e9)
+
+    meta = {"seed": seed, "boost_prob": boost_prob, "boost_amount": boost_amount,
+            "max_depth": [int(tree_depths(parent[b]).max()) for b in range(B)]}
+    return Workload(name, B, N, Hq, Hkv, D, P, V, q, k_tree, v_tree, k_cache, v_cache,
+                    page_table, lens, parent, draft, logits, meta)
+
+
+# --------------------------------------------------------------------------
+# the five named presets
+# --------------------------------------------------------------------------
+
+PRESETS = ("tiny", "llama8b_bs1", "llama8b_bs16", "llama70b_bs8", "long_wide_bs4")
+
+
+def preset(name: str, *, poison: bool = False, with_logits: bool = True,
+           B: int | None = None, boost_amount: float = 3.0) -> Workload:
+    """The five Llama-shaped verification workloads. Preset k (1-based) uses
+    seed k-1. `B` overrides the batch (a bounded sample of the same recipe)."""
+    if name == "tiny":
+        return make_workload(name, 0, B=B or 1, N=16, Hq=8, Hkv=8, D=64, kv_len=128,
+                             parent_fn=lambda r: tree_uniform_forest(r, 16), V=1000,
+                             boost_prob=0.0, distinct_siblings=False, poison=poison,
+                             with_logits=with_logits)
+    if name == "llama8b_bs1":
+        return make_workload(name, 1, B=B or 1, N=64, Hq=32, Hkv=8, D=128, kv_len=2048,
+                             parent_fn=lambda r: tree_topk_expansion(r, (4, 4, 2, 2, 1, 1), 64),
+                             V=128256, boost_prob=0.6, boost_amount=boost_amount,
+                             poison=poison, with_logits=with_logits)
+    if name == "llama8b_bs16":
+        return make_workload(name, 2, B=B or 16, N=64, Hq=32, Hkv=8, D=128,
+                             kv_len=(1024, 4096),
+                             parent_fn=lambda r: tree_random_depth_capped(r, 64, 8),
+                             V=128256, boost_prob=0.6, boost_amount=boost_amount,
+                             poison=poison, with_logits=with_logits)
+    if name == "llama70b_bs8":
+        return make_workload(name, 3, B=B or 8, N=128, Hq=64, Hkv=8, D=128, kv_len=8192,
+                             parent_fn=lambda r: tree_random_depth_capped(r, 128, 10),
+                             V=128256, boost_prob=0.5, boost_amount=boost_amount,
+                             poison=poison, with_logits=with_logits)
+    if name == "long_wide_bs4":
+        return make_workload(name, 4, B=B or 4, N=256, Hq=32, Hkv=8, D=128, kv_len=32768,
+                             parent_fn=lambda r: tree_random_depth_capped(r, 256, 12,
+                                                                          root_children=8),
+                             V=128256, boost_prob=0.4, boost_amount=boost_amount,
+                             poison=poison, with_logits=with_logits)
+    raise KeyError(name)
+
+
+PRESET_DOC = {
+    "tiny": "batch 1, 8/8 heads, head_dim 64, prefix 128, 16-node forest "
+            "(parent uniform in [-1, i-1]), vocab 1000, seed 0",
+    "llama8b_bs1": "batch 1, 32/8 heads, head_dim 128, prefix 2048 in 16-token pages, "
+                   "64-node top-k tree (4,4,2,2,1,1), vocab 128256, +3 boost w.p. 0.6",
+    "llama8b_bs16": "batch 16, 32/8 heads, head_dim 128, prefix U[1024,4096], 64-node "
+                    "random trees (depth <= 8), vocab 128256, +3 boost w.p. 0.6",
+    "llama70b_bs8": "batch 8, 64/8 heads, head_dim 128, prefix 8192, 128-node random trees "
+                    "(depth <= 10), vocab 128256, +3 boost w.p. 0.5",
+    "long_wide_bs4": "batch 4, 32/8 heads, head_dim 128, prefix 32768, 256-node trees "
+                     "(8 root children, depth <= 12), vocab 128256, +3 boost w.p. 0.4",
+}
