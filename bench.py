@@ -1,0 +1,233 @@
+"""Benchmark of one target-model tree-verification step on one MI355X.
+
+A step is the whole hot path on one batch: tree_verify_attention (every
+draft-tree node over its paged prefix plus its root path), tree_argmax_accept
+(vocabulary argmax, greedy longest accepted path, bonus token) and
+kv_compact_accepted (accepted rows into the cache), all through the C ABI on
+one HIP stream. Inputs are resident in HBM before timing starts; consecutive
+steps rotate over several copies of the inputs (more than 1 GB apart) so no
+step finds its data in the 256 MB Infinity Cache.
+
+Prints ONE JSON line. `value` is verified tree-tokens per second (B * N tree
+nodes verified per step / wall time per step). `roofline` describes the
+kernel call that takes the most time; `roofline_attention` the attention
+call. `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import glob
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+METRIC = "verified tree-tokens/sec + achieved HBM GB/s (% of peak), 8B-shaped, 1 GPU"
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2602_21224_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic(w):
+    """Bytes (and FLOP) the method itself must move (and do) per call."""
+    from paper_2602_21224_amd.workloads import tree_depths
+    L = w.kv_len.astype(np.int64)
+    row = w.Hkv * w.D * 2                                     # one K or V row, bf16
+    anc = sum(int((tree_depths(w.parent[b]) + 1).sum()) for b in range(w.B))
+    pages_used = int(sum((int(l) + w.P - 1) // w.P for l in L))
+    attn_bytes = (int(L.sum()) * row * 2                      # prefix K + V
+                  + w.B * w.N * row * 2                       # tree K + V
+                  + 2 * w.B * w.N * w.Hq * w.D * 2            # q in, out
+                  + w.B * w.N * w.Hq * 4                      # lse out
+                  + pages_used * 4 + w.B * w.N * 4 + w.B * 4)  # page ids, parent, kv_len
+    attn_flop = 4 * w.N * w.Hq * w.D * int(L.sum()) + 4 * w.Hq * w.D * anc
+    accept_bytes = w.B * w.N * w.V * 4 + 3 * w.B * w.N * 4 + w.B * w.N * 4 + 2 * w.B * 4
+    return attn_bytes, attn_flop, accept_bytes
+
+
+def compact_bytes(w, accept_len):
+    return 2 * int(accept_len.sum()) * w.Hkv * w.D * 2 * 2    # K and V rows, read + write
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_digest") != source_digest():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, sample_b: int):
+    """The fp64 CPU oracle on the first `sample_b` sequences of the same workload."""
+    import oracle
+    sl = slice(0, sample_b)
+    t0 = time.perf_counter()
+    oracle.tree_attention(w.q[sl], w.k_tree[sl], w.v_tree[sl], w.k_cache, w.v_cache,
+                          w.page_table[sl], w.kv_len[sl], w.parent[sl])
+    a = oracle.argmax(w.logits[sl])
+    alen, aidx, _ = oracle.accept(w.draft[sl], w.parent[sl], a)
+    oracle.kv_compact(w.k_tree[sl], w.v_tree[sl], w.k_cache, w.v_cache, w.page_table[sl],
+                      w.kv_len[sl], aidx, alen)
+    dt = time.perf_counter() - t0
+    return {"value": round(sample_b * w.N / dt, 2), "unit": "verified tree-tokens/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{sample_b} of {w.B} sequences of the same workload "
+                      f"(fp64 C, OpenMP), {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama8b_bs16")
+    ap.add_argument("--copies", type=int, default=3)
+    ap.add_argument("--cpu-sample", type=int, default=-1,
+                    help="sequences in the CPU-oracle sample (-1: all, 0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the verification "
+              "step shards by sequence with no exchange, so N GPUs run N independent copies.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2602_21224_amd as T
+    from paper_2602_21224_amd import workloads as W
+
+    T.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.preset(args.workload)
+    print(f"# workload {args.workload}: B={w.B} N={w.N} Hq={w.Hq} Hkv={w.Hkv} D={w.D} "
+          f"V={w.V} kv_len sum={int(w.kv_len.sum())}", file=sys.stderr, flush=True)
+
+    def up(a, bf16=False):
+        t = torch.from_numpy(np.ascontiguousarray(a.view(np.int16) if bf16 else a))
+        t = t.to(dev)
+        return t.view(torch.bfloat16) if bf16 else t
+
+    base = dict(q=up(w.q, True), k_tree=up(w.k_tree, True), v_tree=up(w.v_tree, True),
+                k_cache=up(w.k_cache, True), v_cache=up(w.v_cache, True),
+                page_table=up(w.page_table), kv_len=up(w.kv_len), parent=up(w.parent),
+                draft=up(w.draft), logits=up(w.logits))
+    copies = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(args.copies - 1)]
+    ws_attn = torch.empty(T.attention_workspace_size(w.B, w.N, w.Hq, w.Hkv, w.D),
+                          dtype=torch.uint8, device=dev)
+    ws_acc = torch.empty(T.argmax_workspace_size(w.B, w.N, w.V), dtype=torch.uint8, device=dev)
+    outs = [dict(out=torch.empty((w.B, w.N, w.Hq, w.D), dtype=torch.bfloat16, device=dev),
+                 lse=torch.empty((w.B, w.N, w.Hq), dtype=torch.float32, device=dev),
+                 amax=torch.empty((w.B, w.N), dtype=torch.int32, device=dev),
+                 alen=torch.empty((w.B,), dtype=torch.int32, device=dev),
+                 aidx=torch.empty((w.B, w.N), dtype=torch.int32, device=dev),
+                 bonus=torch.empty((w.B,), dtype=torch.int32, device=dev))
+            for _ in copies]
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        c, o = copies[i % len(copies)], outs[i % len(copies)]
+        if ev: ev[0].record(stream)
+        T.tree_verify_attention(c["q"], c["k_tree"], c["v_tree"], c["k_cache"], c["v_cache"],
+                                c["page_table"], c["kv_len"], c["parent"],
+                                max_kv_len=w.max_kv_len, out=o["out"], lse=o["lse"],
+                                workspace=ws_attn)
+        if ev: ev[1].record(stream)
+        T.tree_argmax_accept(c["logits"], c["draft"], c["parent"], argmax_out=o["amax"],
+                             accept_len=o["alen"], accept_idx=o["aidx"], bonus_token=o["bonus"],
+                             workspace=ws_acc)
+        if ev: ev[2].record(stream)
+        T.kv_compact_accepted(c["k_tree"], c["v_tree"], c["k_cache"], c["v_cache"],
+                              c["page_table"], c["kv_len"], o["aidx"], o["alen"])
+        if ev: ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    t_attn = np.array([e[0].elapsed_time(e[1]) for e in evs]) * 1e-3
+    t_acc = np.array([e[1].elapsed_time(e[2]) for e in evs]) * 1e-3
+    t_cmp = np.array([e[2].elapsed_time(e[3]) for e in evs]) * 1e-3
+    ms_per_step = wall / args.steps * 1e3
+    tokens = w.B * w.N
+    value = tokens / (wall / args.steps)
+
+    alen = outs[0]["alen"].cpu().numpy()
+    attn_bytes, attn_flop, acc_bytes = algorithmic(w)
+    cmp_bytes = compact_bytes(w, alen)
+    a_attn = attn_bytes / t_attn.mean() / 1e9
+    a_acc = acc_bytes / t_acc.mean() / 1e9
+
+    def roof(kernel, bytes_, t, flop=None):
+        r = {"bound": "hbm", "achieved": round(bytes_ / t / 1e9, 1), "peak": HBM_PEAK_GBS,
+             "unit": "GB/s", "frac": round(bytes_ / t / 1e9 / HBM_PEAK_GBS, 4),
+             "traffic": load_traffic(kernel, args.workload),
+             "kernel": kernel, "avg_us": round(t * 1e6, 2), "algorithmic_bytes": int(bytes_)}
+        if flop is not None:
+            r["tflops"] = round(flop / t / 1e12, 1)
+            r["mfma_frac"] = round(flop / t / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+        return r
+
+    r_attn = roof("tree_verify_attention", attn_bytes, t_attn.mean(), attn_flop)
+    r_acc = roof("tree_argmax_accept", acc_bytes, t_acc.mean())
+    dominant = r_acc if t_acc.mean() >= t_attn.mean() else r_attn
+
+    cpu = None
+    if args.cpu_sample != 0:
+        nb = w.B if args.cpu_sample < 0 else min(args.cpu_sample, w.B)
+        cpu = cpu_baseline(w, nb)
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "verified tree-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "batch": w.B, "tree_nodes": w.N,
+                   "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.D, "page_size": w.P,
+                   "vocab": w.V, "kv_len_sum": int(w.kv_len.sum()),
+                   "kv_len_range": [int(w.kv_len.min()), int(w.kv_len.max())],
+                   "input_copies_rotated": len(copies)},
+        "roofline": dominant,
+        "roofline_attention": r_attn,
+        "step_breakdown_us": {"attention": round(t_attn.mean() * 1e6, 2),
+                              "argmax_accept": round(t_acc.mean() * 1e6, 2),
+                              "compact": round(t_cmp.mean() * 1e6, 2),
+                              "attention_p50": round(float(np.median(t_attn)) * 1e6, 2),
+                              "argmax_accept_p50": round(float(np.median(t_acc)) * 1e6, 2)},
+        "kernel_tokens_per_s": round(tokens / (t_attn.mean() + t_acc.mean() + t_cmp.mean()), 1),
+        "accept_len_hist": np.bincount(alen).tolist(),
+        "compact_bytes": cmp_bytes,
+        "cpu_baseline": cpu,
+        "source_digest": source_digest(),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,206 @@
+/*
+ * treeverify: target-model tree verification on AMD Instinct MI355X (gfx950).
+ *
+ * One verification step of tree-based speculative decoding, as the paper
+ * "Make Every Draft Count: Hidden State based Speculative Decoding" states
+ * it: the target model verifies a draft token tree in one parallel pass
+ * under a tree-shaped attention mask (§2.1; §8 cites SpecInfer's tree
+ * masking), accepts one path of the tree and produces a bonus token (§5.3),
+ * decoding greedily (§7.1: temperature 0), over a paged KV cache (§7.1).
+ * The three calls below are that step's data-parallel part:
+ *
+ *   tree_verify_attention  every node's query heads attend to the sequence's
+ *                          committed prefix and to the node's own root path;
+ *   tree_argmax_accept     per-node vocabulary argmax, greedy longest accepted
+ *                          path, bonus token;
+ *   kv_compact_accepted    the accepted path's K/V rows are written into the
+ *                          cache right after the committed prefix.
+ *
+ * Conventions shared by every call
+ *   - Every pointer argument is a DEVICE pointer, owned by the caller. The
+ *     library never allocates, frees or retains device memory.
+ *   - bf16 tensors are passed as uint16_t bit patterns. Index tensors are
+ *     int32. Every tensor is dense, row-major (C order), in the layout given.
+ *   - Calls are asynchronous on `stream` (0 = the null stream) and never
+ *     synchronize. The return value is a status: TV_OK (0) or a negative
+ *     TV_ERR_* code. Argument checks are done on the host before anything is
+ *     launched; on an error nothing is launched and no output is written.
+ *     TV_ERR_HIP reports a launch failure; asynchronous execution errors
+ *     surface through the HIP runtime as usual.
+ *   - The library keeps no state between calls apart from a per-device cache
+ *     of the compute-unit count. Calls are safe from several host threads as
+ *     long as their output buffers do not overlap.
+ *
+ * Tree format
+ *   Node i of sequence b has parent[b][i] in [-1, i-1] (topological order: a
+ *   parent precedes its children). parent == -1 marks a root: the anchor a
+ *   draft tree hangs from (the last verified token, or the ground-truth token
+ *   a re-sampled tree is rooted at, §5.3 / Alg. 2). Roots are always accepted;
+ *   several roots form a forest. A node sees itself and its ancestors.
+ *
+ * Content contract (not checked in the fast path; tv_validate_inputs checks
+ * it): parent[b][i] in [-1, i-1]; kv_len[b] >= 0; every page id the prefix
+ * and the compacted rows touch lies in [0, num_pages); and
+ * ceil((kv_len[b] + accepted rows) / P) <= max_pages. Kernels clamp or skip
+ * out-of-range ids and never read or write outside the buffers described
+ * here, but results for inputs that break the contract are unspecified.
+ */
+#ifndef TREEVERIFY_H
+#define TREEVERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(TREEVERIFY_BUILD)
+#define TV_API __attribute__((visibility("default")))
+#else
+#define TV_API
+#endif
+
+#define TV_ABI_VERSION 1
+
+enum tv_status {
+    TV_OK = 0,
+    TV_ERR_NULL = -1,        /* a required pointer is NULL                      */
+    TV_ERR_SHAPE = -2,       /* a size or count is outside the supported range  */
+    TV_ERR_ALIGN = -3,       /* a tensor pointer is not 16-byte aligned         */
+    TV_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required      */
+    TV_ERR_HIP = -5,         /* a HIP runtime call or kernel launch failed      */
+    TV_ERR_DEVICE = -6       /* the current device is not gfx950                */
+};
+
+/* TV_ABI_VERSION of the built library. */
+TV_API int tv_abi_version(void);
+
+/* Static English text for a status code (never NULL). */
+TV_API const char *tv_status_string(int status);
+
+/* ------------------------------------------------------------------------
+ * tree_verify_attention
+ *
+ * For sequence b, node i and query head h (KV head g = h / (Hq / Hkv)):
+ *   visible keys  R(b, i) = prefix positions 0 .. kv_len[b]-1
+ *                           U { tree node j : j == i or j is an ancestor of i }
+ *   s_j  = scale * <q[b,i,h,:], k_j[g,:]>
+ *   out[b,i,h,:] = sum_j softmax(s)_j * v_j[g,:]      (bf16, round to nearest even)
+ *   lse[b,i,h]   = log sum_j exp(s_j)                  (fp32, natural log)
+ * Prefix key t of sequence b lives at
+ *   k_cache[page_table[b][t / P]][t % P][g][:]  (v_cache likewise).
+ * Tree node j's own key/value is k_tree[b][j][g][:] / v_tree[b][j][g][:].
+ * (§2.1 tree-shaped attention; §8 tree masking; §1 attention over the cached
+ * prefix; §7.1 paged KV cache.) Keys and values are post-positional-encoding
+ * inputs; positions are the caller's concern.
+ *
+ *   q           [B, N, Hq, D]              bf16
+ *   k_tree      [B, N, Hkv, D]             bf16
+ *   v_tree      [B, N, Hkv, D]             bf16
+ *   k_cache     [num_pages, P, Hkv, D]     bf16
+ *   v_cache     [num_pages, P, Hkv, D]     bf16 (slots past kv_len may hold
+ *                                          anything, NaN included: they are
+ *                                          never read into the result)
+ *   page_table  [B, max_pages]             int32
+ *   kv_len      [B]                        int32, committed prefix lengths
+ *   parent      [B, N]                     int32
+ *   out         [B, N, Hq, D]              bf16, every element written
+ *   lse         [B, N, Hq]                 fp32, or NULL
+ *   workspace   >= tv_attention_workspace_size(...) bytes of device memory,
+ *               16-byte aligned; contents on entry do not matter; clobbered.
+ *
+ * Supported: D in {64, 128}; 1 <= N <= 256; Hq % Hkv == 0 and
+ * (Hq / Hkv) * N <= 2048; 0 <= B <= 1024; P a power of two in [1, 256];
+ * max_pages >= 1; num_pages >= 1.
+ * max_kv_len is a host-side upper bound of kv_len[] used only to size the
+ * launch; results never depend on it (an understated bound costs speed only).
+ * scale <= 0 selects 1/sqrt(D). q, k_tree, v_tree, k_cache, v_cache, out and
+ * workspace must be 16-byte aligned.
+ * ------------------------------------------------------------------------ */
+TV_API size_t tv_attention_workspace_size(int B, int N, int Hq, int Hkv, int D);
+
+TV_API int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree,
+                                 const uint16_t *v_tree, const uint16_t *k_cache,
+                                 const uint16_t *v_cache, const int32_t *page_table,
+                                 const int32_t *kv_len, const int32_t *parent, int B, int N,
+                                 int Hq, int Hkv, int D, int P, int max_pages, int num_pages,
+                                 int max_kv_len, float scale, uint16_t *out, float *lse,
+                                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * tree_argmax_accept
+ *
+ * Greedy verification (§7.1 temperature 0; §5.3 accepted path and bonus
+ * token; Alg. 2 names the bonus the ground-truth token):
+ *   argmax_out[b,i]  = lowest v maximising logits[b,i,v] (IEEE compare, so
+ *                      -0 == +0; a NaN counts as the maximum, the first NaN wins)
+ *   accepted(i)      = parent[i] == -1, or accepted(parent[i]) and
+ *                      draft_tokens[b,i] == argmax_out[b,parent[i]]
+ *   sel              = accepted node of greatest depth (root depth 0),
+ *                      lowest index on a tie
+ *   accept_len[b]    = depth(sel) + 1          (path nodes, root included, >= 1)
+ *   accept_idx[b,:]  = root .. sel node ids, then -1 up to N
+ *   bonus_token[b]   = argmax_out[b, sel]
+ *
+ *   logits        [B, N, V]  fp32 (V * 4 bytes per row; rows need no alignment)
+ *   draft_tokens  [B, N]     int32
+ *   parent        [B, N]     int32
+ *   argmax_out    [B, N]     int32
+ *   accept_len    [B]        int32
+ *   accept_idx    [B, N]     int32
+ *   bonus_token   [B]        int32
+ *   workspace     >= tv_argmax_workspace_size(B, N, V) bytes, 8-byte aligned.
+ * Supported: 0 <= B <= 65535, 1 <= N <= 256, 1 <= V < 2^31.
+ * ------------------------------------------------------------------------ */
+TV_API size_t tv_argmax_workspace_size(int B, int N, int V);
+
+TV_API int tree_argmax_accept(const float *logits, const int32_t *draft_tokens,
+                              const int32_t *parent, int B, int N, int V, int32_t *argmax_out,
+                              int32_t *accept_len, int32_t *accept_idx, int32_t *bonus_token,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * kv_compact_accepted
+ *
+ * Keep the accepted path's keys/values (§1: the KV cache holds committed
+ * tokens; rejected branches are discarded): for j < accept_len[b],
+ *   pos = kv_len[b] + j
+ *   k_cache[page_table[b][pos / P]][pos % P][:][:] = k_tree[b][accept_idx[b,j]][:][:]
+ *   v_cache likewise.
+ * No other cache byte changes. kv_len is NOT modified: the caller advances
+ * it by accept_len after this call. Source and destination never overlap.
+ *
+ *   k_tree, v_tree     [B, N, Hkv, D]          bf16
+ *   k_cache, v_cache   [num_pages, P, Hkv, D]  bf16, written in place
+ *   page_table [B, max_pages], kv_len [B], accept_idx [B, N], accept_len [B] int32
+ * Supported: 0 <= B <= 65535, 1 <= N <= 256, Hkv * D a multiple of 8,
+ * P a power of two in [1, 256]. Rows whose node id or page id is out of
+ * range are skipped (contract violation).
+ * ------------------------------------------------------------------------ */
+TV_API int kv_compact_accepted(const uint16_t *k_tree, const uint16_t *v_tree, uint16_t *k_cache,
+                               uint16_t *v_cache, const int32_t *page_table,
+                               const int32_t *kv_len, const int32_t *accept_idx,
+                               const int32_t *accept_len, int B, int N, int Hkv, int D, int P,
+                               int max_pages, int num_pages, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * tv_validate_inputs (debug aid)
+ *
+ * Checks the content contract on the device and writes a bit set to
+ * *status_word (device int32): bit 0 parent out of [-1, i-1]; bit 1 negative
+ * kv_len; bit 2 a prefix or compaction page index beyond max_pages; bit 3 a
+ * page id the prefix or the N tree rows would use outside [0, num_pages).
+ * 0 means the inputs satisfy the contract for up to N compacted rows.
+ * ------------------------------------------------------------------------ */
+TV_API int tv_validate_inputs(const int32_t *page_table, const int32_t *kv_len,
+                              const int32_t *parent, int B, int N, int P, int max_pages,
+                              int num_pages, int32_t *status_word, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREEVERIFY_H */

@@ -43,6 +43,9 @@ def _load():
         i = ctypes.c_int
         lib.oracle_tree_attention.argtypes = [p] * 8 + [i] * 8 + [ctypes.c_double, p, p]
         lib.oracle_tree_attention.restype = i
+        lib.oracle_tree_attention_rows.argtypes = [p] * 8 + [i] * 8 + [ctypes.c_double, p, i,
+                                                                        p, p]
+        lib.oracle_tree_attention_rows.restype = i
         lib.oracle_argmax.argtypes = [p, ctypes.c_long, ctypes.c_long, p]
         lib.oracle_argmax.restype = None
         lib.oracle_accept.argtypes = [p, p, p, i, i, p, p, p]
@@ -94,6 +97,33 @@ def tree_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, pare
         float(scale), _ptr(out), _ptr(lse))
     if rc != 0:
         raise ValueError("oracle_tree_attention rejected its arguments")
+    return out, lse
+
+
+def tree_attention_rows(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, items,
+                        scale: float = 0.0):
+    """The same attention for selected (b, i, h) rows only; items is an int
+    array [n, 3]. Returns (out [n, D], lse [n]) in fp64."""
+    q = _c(q, np.uint16)
+    k_tree = _c(k_tree, np.uint16)
+    v_tree = _c(v_tree, np.uint16)
+    k_cache = _c(k_cache, np.uint16)
+    v_cache = _c(v_cache, np.uint16)
+    page_table = _c(page_table, np.int32)
+    kv_len = _c(kv_len, np.int32)
+    parent = _c(parent, np.int32)
+    items = _c(items, np.int32).reshape(-1, 3)
+    B, N, Hq, D = q.shape
+    Hkv = k_tree.shape[2]
+    num_pages, P = k_cache.shape[0], k_cache.shape[1]
+    out = np.zeros((len(items), D), dtype=np.float64)
+    lse = np.zeros(len(items), dtype=np.float64)
+    rc = _load().oracle_tree_attention_rows(
+        _ptr(q), _ptr(k_tree), _ptr(v_tree), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
+        _ptr(kv_len), _ptr(parent), B, N, Hq, Hkv, D, P, page_table.shape[1], num_pages,
+        float(scale), _ptr(items), len(items), _ptr(out), _ptr(lse))
+    if rc != 0:
+        raise ValueError("oracle_tree_attention_rows rejected its arguments")
     return out, lse
 
 

@@ -66,10 +66,99 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Argument checks shared by the attention entry points. */
+static int attention_args_ok(const int32_t *page_table, const int32_t *kv_len,
+                             const int32_t *parent, int B, int N, int Hq, int Hkv, int D, int P,
+                             int max_pages, int num_pages)
+{
+    if (B < 0 || N < 1 || Hq < 1 || Hkv < 1 || D < 1 || P < 1 || Hq % Hkv != 0)
+        return 0;
+    for (int b = 0; b < B; ++b) {
+        int L = kv_len[b];
+        if (L < 0 || (L + P - 1) / P > max_pages)
+            return 0;
+        for (int t = 0; t < L; t += P) {
+            int pg = page_table[(long)b * max_pages + t / P];
+            if (pg < 0 || pg >= num_pages)
+                return 0;
+        }
+        for (int i = 0; i < N; ++i) {
+            int p = parent[(long)b * N + i];
+            if (p < -1 || p >= i)
+                return 0;
+        }
+    }
+    return 1;
+}
+
+/* One output row: node i of sequence b, query head h. Writes D values to o
+ * and the log-sum-exp to *lse_out (if not NULL). */
+static void attend_one(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
+                       const uint16_t *k_cache, const uint16_t *v_cache,
+                       const int32_t *page_table, const int32_t *kv_len, const int32_t *parent,
+                       int N, int Hq, int Hkv, int D, int P, int max_pages, double scale, int b,
+                       int i, int h, double *o, double *lse_out)
+{
+    const int G = Hq / Hkv;
+    const int g = h / G;
+    const int L = kv_len[b];
+    const uint16_t *qrow = q + (((long)b * N + i) * Hq + h) * D;
+
+    /* visible keys: the L prefix positions, then node i and its ancestors */
+    int nvis = L;
+    for (int j = i; j >= 0; j = parent[(long)b * N + j])
+        ++nvis;
+    const uint16_t **krow = malloc(sizeof(*krow) * (size_t)nvis);
+    const uint16_t **vrow = malloc(sizeof(*vrow) * (size_t)nvis);
+    double *s = malloc(sizeof(double) * (size_t)nvis);
+
+    int n = 0;
+    for (int t = 0; t < L; ++t) {
+        long pg = page_table[(long)b * max_pages + t / P];
+        long off = ((pg * P + t % P) * Hkv + g) * D;
+        krow[n] = k_cache + off;
+        vrow[n] = v_cache + off;
+        ++n;
+    }
+    for (int j = i; j >= 0; j = parent[(long)b * N + j]) {
+        long off = (((long)b * N + j) * Hkv + g) * D;
+        krow[n] = k_tree + off;
+        vrow[n] = v_tree + off;
+        ++n;
+    }
+
+    /* scores and their maximum */
+    double m = -INFINITY;
+    for (int j = 0; j < n; ++j) {
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d)
+            dot += widen_bf16(qrow[d]) * widen_bf16(krow[j][d]);
+        s[j] = scale * dot;
+        if (s[j] > m)
+            m = s[j];
+    }
+    /* softmax-weighted sum of values */
+    double denom = 0.0;
+    for (int j = 0; j < n; ++j) {
+        s[j] = exp(s[j] - m);
+        denom += s[j];
+    }
+    for (int d = 0; d < D; ++d) {
+        double acc = 0.0;
+        for (int j = 0; j < n; ++j)
+            acc += s[j] * widen_bf16(vrow[j][d]);
+        o[d] = acc / denom;
+    }
+    if (lse_out)
+        *lse_out = m + log(denom);
+    free(krow);
+    free(vrow);
+    free(s);
+}
+
 /* Tree-masked attention of every node's query heads over the paged prefix
  * plus the node's own root path. Outputs are fp64:
- *   out [B, N, Hq, D], lse [B, N, Hq] (natural log of the softmax denominator
- *   including the max shift, i.e. log sum_j exp(s_j)).
+ *   out [B, N, Hq, D], lse [B, N, Hq] (natural log of sum_j exp(s_j)).
  * Returns 0, or -1 on a malformed argument (nothing written). */
 int oracle_tree_attention(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
                           const uint16_t *k_cache, const uint16_t *v_cache,
@@ -78,87 +167,50 @@ int oracle_tree_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
                           int P, int max_pages, int num_pages, double scale,
                           double *out, double *lse)
 {
-    if (B < 0 || N < 1 || Hq < 1 || Hkv < 1 || D < 1 || P < 1 || Hq % Hkv != 0)
+    if (!attention_args_ok(page_table, kv_len, parent, B, N, Hq, Hkv, D, P, max_pages, num_pages))
         return -1;
-    for (int b = 0; b < B; ++b) {
-        int L = kv_len[b];
-        if (L < 0 || (L + P - 1) / P > max_pages)
-            return -1;
-        for (int t = 0; t < L; t += P) {
-            int pg = page_table[(long)b * max_pages + t / P];
-            if (pg < 0 || pg >= num_pages)
-                return -1;
-        }
-        for (int i = 0; i < N; ++i) {
-            int p = parent[(long)b * N + i];
-            if (p < -1 || p >= i)
-                return -1;
-        }
-    }
     if (!(scale > 0.0))
         scale = 1.0 / sqrt((double)D);
-    const int G = Hq / Hkv;
 
 #pragma omp parallel for collapse(3) schedule(dynamic, 4)
     for (int b = 0; b < B; ++b)
         for (int i = 0; i < N; ++i)
             for (int h = 0; h < Hq; ++h) {
-                const int g = h / G;
-                const int L = kv_len[b];
-                const uint16_t *qrow = q + (((long)b * N + i) * Hq + h) * D;
-
-                /* visible keys: the L prefix positions, then node i and its ancestors */
-                int nvis = L;
-                for (int j = i; j >= 0; j = parent[(long)b * N + j])
-                    ++nvis;
-                const uint16_t **krow = malloc(sizeof(*krow) * (size_t)nvis);
-                const uint16_t **vrow = malloc(sizeof(*vrow) * (size_t)nvis);
-                double *s = malloc(sizeof(double) * (size_t)nvis);
-
-                int n = 0;
-                for (int t = 0; t < L; ++t) {
-                    long pg = page_table[(long)b * max_pages + t / P];
-                    long off = ((pg * P + t % P) * Hkv + g) * D;
-                    krow[n] = k_cache + off;
-                    vrow[n] = v_cache + off;
-                    ++n;
-                }
-                for (int j = i; j >= 0; j = parent[(long)b * N + j]) {
-                    long off = (((long)b * N + j) * Hkv + g) * D;
-                    krow[n] = k_tree + off;
-                    vrow[n] = v_tree + off;
-                    ++n;
-                }
-
-                /* scores and their maximum */
-                double m = -INFINITY;
-                for (int j = 0; j < n; ++j) {
-                    double dot = 0.0;
-                    for (int d = 0; d < D; ++d)
-                        dot += widen_bf16(qrow[d]) * widen_bf16(krow[j][d]);
-                    s[j] = scale * dot;
-                    if (s[j] > m)
-                        m = s[j];
-                }
-                /* softmax-weighted sum of values */
-                double denom = 0.0;
-                for (int j = 0; j < n; ++j) {
-                    s[j] = exp(s[j] - m);
-                    denom += s[j];
-                }
-                double *o = out + (((long)b * N + i) * Hq + h) * D;
-                for (int d = 0; d < D; ++d) {
-                    double acc = 0.0;
-                    for (int j = 0; j < n; ++j)
-                        acc += s[j] * widen_bf16(vrow[j][d]);
-                    o[d] = acc / denom;
-                }
-                if (lse)
-                    lse[((long)b * N + i) * Hq + h] = m + log(denom);
-                free(krow);
-                free(vrow);
-                free(s);
+                long row = ((long)b * N + i) * Hq + h;
+                attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, N,
+                           Hq, Hkv, D, P, max_pages, scale, b, i, h, out + row * D,
+                           lse ? lse + row : NULL);
             }
+    return 0;
+}
+
+/* The same attention for a list of n_items (b, i, h) triples only (items is
+ * [n_items][3]); row k of out_rows [n_items, D] and lse_rows [n_items]
+ * belongs to item k. Used to check large workloads on sampled outputs. */
+int oracle_tree_attention_rows(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
+                               const uint16_t *k_cache, const uint16_t *v_cache,
+                               const int32_t *page_table, const int32_t *kv_len,
+                               const int32_t *parent, int B, int N, int Hq, int Hkv, int D, int P,
+                               int max_pages, int num_pages, double scale, const int32_t *items,
+                               int n_items, double *out_rows, double *lse_rows)
+{
+    if (!attention_args_ok(page_table, kv_len, parent, B, N, Hq, Hkv, D, P, max_pages, num_pages))
+        return -1;
+    for (int k = 0; k < n_items; ++k) {
+        const int32_t *it = items + 3L * k;
+        if (it[0] < 0 || it[0] >= B || it[1] < 0 || it[1] >= N || it[2] < 0 || it[2] >= Hq)
+            return -1;
+    }
+    if (!(scale > 0.0))
+        scale = 1.0 / sqrt((double)D);
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int k = 0; k < n_items; ++k) {
+        const int32_t *it = items + 3L * k;
+        attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, N, Hq, Hkv,
+                   D, P, max_pages, scale, it[0], it[1], it[2], out_rows + (long)k * D,
+                   lse_rows ? lse_rows + k : NULL);
+    }
     return 0;
 }
 

@@ -1,0 +1,17 @@
+"""Target-model tree verification for MI355X (gfx950): HIP kernels behind a C ABI.
+
+The entry points are re-exported lazily from `_lib` so that importing the
+package (for example to draw synthetic workloads) does not need the built
+library.
+"""
+
+__all__ = ["tree_verify_attention", "tree_argmax_accept", "kv_compact_accepted",
+           "tv_validate_inputs", "attention_workspace_size", "argmax_workspace_size",
+           "abi_version", "load"]
+
+
+def __getattr__(name):
+    if name in __all__:
+        from . import _lib
+        return getattr(_lib, name)
+    raise AttributeError(name)

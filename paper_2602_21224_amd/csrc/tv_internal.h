@@ -1,0 +1,64 @@
+// Internal declarations shared by the HIP sources of libtreeverify (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kNumXcd = 8;           // MI355X: 8 XCDs, workgroups dispatched round-robin
+constexpr int kKeyTile = 64;         // keys per attention tile (two 32-key MFMA blocks)
+constexpr int kRowsPerWave = 32;     // query rows per wave (MFMA N dimension)
+constexpr int kMaxNodes = 256;
+constexpr int kMaxBatchAttn = 1024;
+
+// Launch parameters of the tree-attention kernels (all sizes in elements).
+struct AttnParams {
+    const uint16_t *q, *k_tree, *v_tree, *k_cache, *v_cache;
+    const int32_t *page_table, *kv_len, *parent;
+    uint16_t *out;
+    float *lse;
+    float *ws_o;       // [num_wg * 2][rows_per_block][D] partial numerators
+    float *ws_ml;      // [num_wg * 2][rows_per_block][2] partial (max, sum)
+    int32_t *ws_cum;   // [B + 1] cumulative tile counts (written by workgroup 0)
+    int B, N, Hq, Hkv, G, rows, P, p_shift, max_pages, num_pages;
+    int rows_per_block, row_blocks;
+    int tree_tiles_all_blocks;   // sum over row blocks of the tree tiles each needs
+    int num_wg;
+    float scale_log2;            // softmax scale * log2(e)
+    float scale;                 // softmax scale
+};
+
+// Workgroup -> logical index remap: the hardware hands consecutive workgroup
+// ids to consecutive XCDs; give every XCD one contiguous run of logical ids
+// so neighbouring work (which shares K/V rows) shares that XCD's L2.
+__device__ __forceinline__ int xcd_contiguous_id(int hw_id, int n) {
+    const int xcd = hw_id % kNumXcd;
+    const int local = hw_id / kNumXcd;
+    const int base = xcd * (n / kNumXcd) + min(xcd, n % kNumXcd);
+    return base + local;
+}
+
+// Host-side launchers (defined next to their kernels).
+hipError_t launch_tree_attention(const AttnParams &p, int head_dim, int waves, hipStream_t s);
+hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const int32_t *parent,
+                                int B, int N, int V, int segs, int seg_len, int32_t *argmax_out,
+                                int32_t *accept_len, int32_t *accept_idx, int32_t *bonus,
+                                unsigned long long *ws, hipStream_t s);
+hipError_t launch_kv_compact(const uint16_t *k_tree, const uint16_t *v_tree, uint16_t *k_cache,
+                             uint16_t *v_cache, const int32_t *page_table, const int32_t *kv_len,
+                             const int32_t *accept_idx, const int32_t *accept_len, int B, int N,
+                             int Hkv, int D, int P, int max_pages, int num_pages, hipStream_t s);
+hipError_t launch_validate(const int32_t *page_table, const int32_t *kv_len,
+                           const int32_t *parent, int B, int N, int P, int max_pages,
+                           int num_pages, int32_t *status_word, hipStream_t s);
+
+}  // namespace tv

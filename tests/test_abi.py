@@ -1,0 +1,112 @@
+"""Host-side checks of the C ABI (CPU only; no kernel is ever launched).
+
+The library loads, exports every function its header declares, and rejects
+malformed arguments on the host with the documented status before touching
+the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "treeverify.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2602_21224_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2602_21224_amd import build
+        build.build()
+    return _lib.load()
+
+
+def declared():
+    text = open(HEADER).read()
+    return re.findall(r"TV_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)
+
+
+def test_header_declares_the_three_calls():
+    names = set(declared())
+    assert {"tree_verify_attention", "tree_argmax_accept", "kv_compact_accepted"} <= names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared():
+        assert hasattr(lib, name), name
+
+
+def test_only_declared_symbols_are_exported():
+    import subprocess
+    from paper_2602_21224_amd import _lib
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if l.split()[1] == "T"}
+    assert exported == set(declared())
+
+
+def test_status_strings(lib):
+    assert lib.tv_abi_version() == 1
+    for code in range(0, -7, -1):
+        assert lib.tv_status_string(code)
+    assert lib.tv_status_string(-99) == b"unknown status"
+
+
+FAKE = ctypes.c_void_p(0x10000)          # never dereferenced: checks return first
+NULL = ctypes.c_void_p(0)
+STREAM = ctypes.c_void_p(0)
+
+
+def attn(lib, **kw):
+    a = dict(q=FAKE, k_tree=FAKE, v_tree=FAKE, k_cache=FAKE, v_cache=FAKE, page_table=FAKE,
+             kv_len=FAKE, parent=FAKE, B=2, N=8, Hq=8, Hkv=2, D=128, P=16, max_pages=4,
+             num_pages=8, max_kv_len=32, scale=0.0, out=FAKE, lse=NULL, ws=FAKE,
+             ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.tree_verify_attention(*a.values(), STREAM)
+
+
+def test_attention_argument_checks(lib):
+    assert attn(lib, B=0) == 0
+    assert attn(lib, q=NULL) == -1
+    assert attn(lib, ws=NULL) == -1
+    assert attn(lib, D=96) == -2
+    assert attn(lib, N=0) == -2 and attn(lib, N=257) == -2
+    assert attn(lib, Hq=6, Hkv=4) == -2
+    assert attn(lib, P=12) == -2
+    assert attn(lib, Hq=64, Hkv=2, N=128) == -2          # more than 2048 rows per KV head
+    assert attn(lib, B=5000) == -2
+    assert attn(lib, q=ctypes.c_void_p(0x10008)) == -3
+    # well-formed on a machine without a GPU: stops at the device check, launches nothing
+    assert attn(lib) in (-4, -6)
+
+
+def test_workspace_size_is_monotone_and_rejects_bad_shapes(lib):
+    small = lib.tv_attention_workspace_size(1, 16, 8, 8, 64)
+    big = lib.tv_attention_workspace_size(16, 64, 32, 8, 128)
+    assert 0 < small < big
+    assert lib.tv_attention_workspace_size(1, 16, 8, 8, 80) == 0
+    assert lib.tv_argmax_workspace_size(16, 64, 128256) >= 16 * 64 * 8
+    assert lib.tv_argmax_workspace_size(1, 0, 10) == 0
+
+
+def test_accept_and_compact_argument_checks(lib):
+    acc = lambda **kw: lib.tree_argmax_accept(*{**dict(l=FAKE, d=FAKE, p=FAKE, B=2, N=4, V=100,
+                                                        a=FAKE, al=FAKE, ai=FAKE, b=FAKE,
+                                                        ws=FAKE, wsb=1 << 30), **kw}.values(),
+                                              STREAM)
+    assert acc(B=0) == 0
+    assert acc(l=NULL) == -1
+    assert acc(N=300) == -2 and acc(V=0) == -2
+    assert acc(wsb=8) == -4
+    assert acc(l=ctypes.c_void_p(0x10002)) == -3
+    cmp_ = lambda **kw: lib.kv_compact_accepted(*{**dict(kt=FAKE, vt=FAKE, kc=FAKE, vc=FAKE,
+                                                          pt=FAKE, kl=FAKE, ai=FAKE, al=FAKE,
+                                                          B=2, N=4, Hkv=8, D=128, P=16, mp=4,
+                                                          np_=8), **kw}.values(), STREAM)
+    assert cmp_(B=0) == 0
+    assert cmp_(kc=NULL) == -1
+    assert cmp_(P=3) == -2
+    assert cmp_(Hkv=1, D=6) == -2
+    assert cmp_(kt=ctypes.c_void_p(0x10004)) == -3

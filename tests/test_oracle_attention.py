@@ -233,3 +233,14 @@ def test_rejects_malformed_tree(oracle_mod):
     bad[0, 2] = 2
     with pytest.raises(ValueError):
         run(oracle_mod, w, parent=bad)
+
+
+def test_rows_entry_matches_full(oracle_mod):
+    w = small(81, B=3, N=11, Hq=8, Hkv=2, D=32, L=(0, 45), P=4, poison=True)
+    out, lse = run(oracle_mod, w)
+    rng = np.random.default_rng(0)
+    items = np.stack([rng.integers(0, 3, 40), rng.integers(0, 11, 40), rng.integers(0, 8, 40)], 1)
+    o2, l2 = oracle_mod.tree_attention_rows(w.q, w.k_tree, w.v_tree, w.k_cache, w.v_cache,
+                                            w.page_table, w.kv_len, w.parent, items)
+    np.testing.assert_array_equal(o2, out[items[:, 0], items[:, 1], items[:, 2]])
+    np.testing.assert_array_equal(l2, lse[items[:, 0], items[:, 1], items[:, 2]])
