@@ -48,7 +48,7 @@ namespace {
 
 constexpr int KT = kKeyTile;           // 64 keys per tile
 constexpr int NS = 4;                  // ring stages
-constexpr int kPageCache = 2048;       // page ids cached in LDS per segment window
+constexpr int kPageCache = 1024;       // page ids cached in LDS per segment window
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr float kRescaleSlack = 8.f;   // keep a stale running max while new scores stay within 2^8 of it
@@ -66,10 +66,34 @@ struct Geo {
     static constexpr int kKeysPerBlock = 1024 / kRowBytes;
 };
 
+// Chunk swizzle of a key row: 16-byte chunk c of key k lives at position
+// c ^ swz(k % chunks). swz swaps the two low bit-fields of the key so that both
+// MFMA operand read patterns are free of LDS bank conflicts: 16 consecutive
+// keys at one chunk (K fragments), and 4 consecutive keys x 4 adjacent chunks
+// (the transposing V reads). It is a bit permutation, so swz(a ^ b) =
+// swz(a) ^ swz(b).
+template <int C>
+__device__ __forceinline__ constexpr int swz(int k) {
+    static_assert(C == 8 || C == 16, "rows of 64 or 128 bf16");
+    return C == 16 ? (((k & 3) << 2) | ((k >> 2) & 3)) : (((k & 3) << 1) | ((k >> 2) & 1));
+}
+
+// Combine a per-row value held by lanes l and l ^ 32 (the two halves of a
+// 32x32 MFMA tile column) without going through LDS.
+__device__ __forceinline__ float halves_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // LDS objects are separate so the compiler can see that only `g_ring` is a
 // target of the asynchronous tile loads.
 __shared__ __attribute__((aligned(1024))) unsigned char g_ring[NS * Geo<128>::kStageBytes];
 __shared__ unsigned long long g_anc[kMaxNodes][4];
+__shared__ unsigned long long g_anc_alt[kMaxNodes][4];
 __shared__ int g_par[kMaxNodes];
 __shared__ int g_jump[2][kMaxNodes];
 __shared__ int g_pages[kPageCache];
@@ -93,6 +117,17 @@ __device__ __forceinline__ int tree_tiles_of_block(int rb, const AttnParams &p) 
 __device__ __forceinline__ int tiles_of_sequence(int b, const AttnParams &p) {
     const int L = clamp_len(p.kv_len[b], p);
     return p.Hkv * (p.row_blocks * ((L + KT - 1) / KT) + p.tree_tiles_all_blocks);
+}
+
+// Explicit LDS wait for reads issued through inline assembly; `tie` makes a
+// fragment's later uses depend on the wait (volatile asm keeps its order).
+template <int N>
+__device__ __forceinline__ void lds_wait() {
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+template <typename T>
+__device__ __forceinline__ void tie(T &x) {
+    asm volatile("" : "+v"(x));
 }
 
 __device__ __forceinline__ void lds_barrier() {
@@ -146,26 +181,59 @@ __device__ void build_cumulative(const AttnParams &p) {
     __syncthreads();
 }
 
-// Ancestor bit sets of the N nodes of sequence b by pointer doubling: after
-// round k, a node's set holds every ancestor within distance < 2^k. The second
-// buffer of the ping-pong lives in the (idle) tile ring. Result in g_anc.
+// Segment set-up, part 1: page ids of pages [first, first + kPageCache) of
+// sequence b (as far as it has them) into g_pages, and the parent links of
+// sequence b into g_par. All loads are issued before any is waited for.
 template <int NT>
-__device__ void build_ancestor_masks(const AttnParams &p, int b) {
+__device__ void load_pages_and_parents(const AttnParams &p, int b, int first, int npages,
+                                       bool want_pages, bool want_parents) {
+    constexpr int PPT = (kPageCache + NT - 1) / NT;
     const int tid = threadIdx.x;
-    unsigned long long(*alt)[4] = reinterpret_cast<unsigned long long(*)[4]>(g_ring);
+    const int n = want_pages ? min(kPageCache, npages - first) : 0;
+    int pg[PPT];
+    #pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+        const int i = tid + k * NT;
+        pg[k] = i < n ? p.page_table[(size_t)b * p.max_pages + first + i] : -1;
+    }
+    int par[(kMaxNodes + NT - 1) / NT];
+    #pragma unroll
+    for (int k = 0; k < (kMaxNodes + NT - 1) / NT; ++k) {
+        const int i = tid + k * NT;
+        par[k] = (want_parents && i < p.N) ? p.parent[(size_t)b * p.N + i] : -1;
+    }
+    #pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+        const int i = tid + k * NT;
+        if (i < n) g_pages[i] = (pg[k] >= 0 && pg[k] < p.num_pages) ? pg[k] : -1;
+    }
+    #pragma unroll
+    for (int k = 0; k < (kMaxNodes + NT - 1) / NT; ++k) {
+        const int i = tid + k * NT;
+        if (want_parents && i < p.N) {
+            const int pi = par[k];
+            g_par[i] = (pi < -1 || pi >= i) ? -1 : pi;   // contract violation: treat as a root
+        }
+    }
+    __syncthreads();
+}
+
+// Segment set-up, part 2: ancestor bit sets of the N nodes (from g_par) by
+// pointer doubling: after round k a node's set holds every ancestor within
+// distance < 2^k. Runs while the first tiles are in flight. Result in g_anc.
+template <int NT>
+__device__ void build_ancestor_masks(const AttnParams &p) {
+    const int tid = threadIdx.x;
     for (int i = tid; i < p.N; i += NT) {
-        int pi = p.parent[(size_t)b * p.N + i];
-        if (pi < -1 || pi >= i) pi = -1;                 // contract violation: treat as a root
-        g_par[i] = pi;
         #pragma unroll
         for (int w = 0; w < 4; ++w) g_anc[i][w] = (w == (i >> 6)) ? (1ull << (i & 63)) : 0ull;
-        g_jump[0][i] = pi;
+        g_jump[0][i] = g_par[i];
     }
     __syncthreads();
     int cur = 0;
     for (int round = 0; round < 8; ++round) {
-        unsigned long long(*src)[4] = cur == 0 ? g_anc : alt;
-        unsigned long long(*dst)[4] = cur == 0 ? alt : g_anc;
+        unsigned long long(*src)[4] = cur == 0 ? g_anc : g_anc_alt;
+        unsigned long long(*dst)[4] = cur == 0 ? g_anc_alt : g_anc;
         int more = 0;
         for (int i = tid; i < p.N; i += NT) {
             const int j = g_jump[cur][i];
@@ -184,37 +252,43 @@ __device__ void build_ancestor_masks(const AttnParams &p, int b) {
         cur ^= 1;
         if (!__syncthreads_or(more)) break;
     }
-    if (cur == 1) {                                      // final sets are in the ring copy
+    if (cur == 1) {
         for (int i = tid; i < p.N; i += NT)
             #pragma unroll
-            for (int w = 0; w < 4; ++w) g_anc[i][w] = alt[i][w];
+            for (int w = 0; w < 4; ++w) g_anc[i][w] = g_anc_alt[i][w];
         __syncthreads();
     }
 }
 
-// Load the page ids of pages [first, first + kPageCache) of sequence b (as far
-// as the sequence has them) into g_pages. Called with no tile loads in flight
-// that this wave still needs to count precisely (it drains vmcnt).
-template <int NT>
-__device__ void load_page_window(const AttnParams &p, int b, int first, int npages) {
-    const int n = min(kPageCache, npages - first);
-    for (int i = threadIdx.x; i < n; i += NT) {
-        const int pg = p.page_table[(size_t)b * p.max_pages + first + i];
-        g_pages[i] = (pg >= 0 && pg < p.num_pages) ? pg : -1;
-    }
-    __syncthreads();
-}
-
 template <int D, int NW>
 struct TileIssue {
-    static constexpr int NT = NW * kWave;
-    static constexpr int kLoadsPerWave = 2 * Geo<D>::kBlocksPerTile / NW;
+    using Gm = Geo<D>;
+    static constexpr int kLoadsPerWave = 2 * Gm::kBlocksPerTile / NW;
+    static constexpr int KPB = Gm::kKeysPerBlock;     // keys per 1 KB load block
+    static constexpr int C = Gm::kChunks;
 
-    // Issue the direct-to-LDS loads of tile t of unit (b, g) into ring stage `stage`.
-    static __device__ __forceinline__ void issue(const AttnParams &p, int b, int g, int L,
-                                                 int ntp, int t, int stage, int page_first,
-                                                 int wave_u, int lane) {
-        using Gm = Geo<D>;
+    int kib;                                          // this lane's key within a block
+    unsigned row_off;                                 // kib * key row stride (bytes)
+    unsigned chunk_off[kLoadsPerWave];                // swizzled chunk offset per load
+
+    __device__ __forceinline__ void init(int wave_u, int lane, unsigned row_stride) {
+        kib = lane / C;
+        row_off = kib * row_stride;
+        #pragma unroll
+        for (int i = 0; i < kLoadsPerWave; ++i) {
+            const int kb = (wave_u * kLoadsPerWave + i) % Gm::kBlocksPerTile;
+            chunk_off[i] = (unsigned)(((lane % C) ^ swz<C>((kb * KPB + kib) % C)) * 16);
+        }
+    }
+
+    // Issue the direct-to-LDS loads of tile t of unit (b, g) into ring stage
+    // `stage`. A load block covers KPB consecutive keys; when a page holds at
+    // least KPB keys they share one page, so the block's base address is
+    // wave-uniform (scalar math) and lanes only add their row/chunk offset.
+    // Rows that do not exist (past the prefix, past N) re-read the block's
+    // first row, or tree node 0 when the whole block is past the end.
+    __device__ __forceinline__ void issue(const AttnParams &p, int b, int g, int L, int ntp,
+                                          int t, int stage, int page_first, int wave_u) const {
         const uint16_t *safe_k = p.k_tree + ((size_t)b * p.N * p.Hkv + g) * D;
         const uint16_t *safe_v = p.v_tree + ((size_t)b * p.N * p.Hkv + g) * D;
         #pragma unroll
@@ -222,27 +296,41 @@ struct TileIssue {
             const int blk = wave_u * kLoadsPerWave + i;                 // wave-uniform
             const bool is_v = blk >= Gm::kBlocksPerTile;
             const int kb = is_v ? blk - Gm::kBlocksPerTile : blk;
-            const int key = kb * Gm::kKeysPerBlock + lane / Gm::kChunks;
-            const int chunk = (lane % Gm::kChunks) ^ (key % Gm::kChunks);
-            const uint16_t *row;
+            const uint16_t *base = is_v ? safe_v : safe_k;
+            const char *addr;
             if (t < ntp) {
-                const int pos = t * KT + key;
-                row = is_v ? safe_v : safe_k;
-                if (pos < L) {
-                    const int pg = g_pages[(pos >> p.p_shift) - page_first];
-                    if (pg >= 0) {
-                        const size_t off = ((((size_t)pg << p.p_shift) + (pos & (p.P - 1))) * p.Hkv + g) * D;
-                        row = (is_v ? p.v_cache : p.k_cache) + off;
+                const int pos0 = t * KT + kb * KPB;
+                const int n_valid = min(max(L - pos0, 0), KPB);
+                if (!p.small_pages) {
+                    int pg = -1;
+                    if (n_valid > 0)
+                        pg = __builtin_amdgcn_readfirstlane(g_pages[(pos0 >> p.p_shift) - page_first]);
+                    const bool ok = pg >= 0;
+                    if (ok)
+                        base = (is_v ? p.v_cache : p.k_cache) +
+                               ((((size_t)pg << p.p_shift) + (pos0 & (p.P - 1))) * p.Hkv + g) * D;
+                    addr = reinterpret_cast<const char *>(base) +
+                           ((ok && kib < n_valid ? row_off : 0u) + chunk_off[i]);
+                } else {
+                    // pages shorter than a load block: every lane finds its own page
+                    const int pos = pos0 + kib;
+                    const uint16_t *row = base;
+                    if (kib < n_valid) {
+                        const int pg = g_pages[(pos >> p.p_shift) - page_first];
+                        if (pg >= 0)
+                            row = (is_v ? p.v_cache : p.k_cache) +
+                                  ((((size_t)pg << p.p_shift) + (pos & (p.P - 1))) * p.Hkv + g) * D;
                     }
+                    addr = reinterpret_cast<const char *>(row) + chunk_off[i];
                 }
             } else {
-                const int j = (t - ntp) * KT + key;
-                row = is_v ? safe_v : safe_k;
-                if (j < p.N) row += (size_t)j * p.Hkv * D;
+                const int j0 = (t - ntp) * KT + kb * KPB;
+                const int n_valid = min(max(p.N - j0, 0), KPB);
+                if (n_valid > 0) base += (size_t)j0 * p.Hkv * D;
+                addr = reinterpret_cast<const char *>(base) + ((kib < n_valid ? row_off : 0u) + chunk_off[i]);
             }
             unsigned char *dst = g_ring + stage * Gm::kStageBytes + (is_v ? Gm::kTileBytes : 0) + kb * 1024;
-            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(row + chunk * 8),
-                                             (LDS_AS void *)dst, 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)addr, (LDS_AS void *)dst, 16, 0, 0);
         }
     }
 };
@@ -272,6 +360,14 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
     const int start = min(w * share, total);
     const int end = min(start + share, total);
     const unsigned ring_base = lds_addr(g_ring);
+    Issue ld;
+    ld.init(wave_u, lane, (unsigned)(p.Hkv * D * 2));
+
+    // lane-constant parts of the LDS fragment addresses (see swz)
+    const unsigned k_lane = col * Gm::kRowBytes + ((half ^ swz<Gm::kChunks>(col % Gm::kChunks)) << 4);
+    const int va = ((lane >> 4) & 1) * 2 + ((lane & 3) >> 1);
+    const int vb = half * 4 + ((lane & 15) >> 2);
+    const unsigned v_lane = vb * Gm::kRowBytes + ((va ^ swz<Gm::kChunks>(vb)) << 4) + (lane & 1) * 8;
 
     int pos = start;
     int seg_no = 0;
@@ -300,7 +396,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         const int t_end = min(ulen, off + (end - pos));
         const bool complete = (t_begin == 0 && t_end == ulen);
 
-        // ---- this wave's query rows: Q fragments stay in registers
+        // ---- this wave's 32 query rows: Q fragments stay in registers
         const int row = rb * p.rows_per_block + wave_u * kRowsPerWave + col;
         const bool row_ok = row < p.rows;
         const int node = row_ok ? row / p.G : 0;
@@ -316,10 +412,11 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             }
         }
 
-        if (t_end > ntp) build_ancestor_masks<NT>(p, b);
+        // ---- page ids and parent links (one round trip), then the first tiles
         const int npages = (L + p.P - 1) >> p.p_shift;
         int page_first = (t_begin * KT) >> p.p_shift;
-        if (t_begin < ntp) load_page_window<NT>(p, b, page_first, npages);
+        const bool has_tree = t_end > ntp;
+        load_pages_and_parents<NT>(p, b, page_first, npages, t_begin < ntp, has_tree);
 
         f32x16 o[NDT];
         #pragma unroll
@@ -329,12 +426,12 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         float m_run = kNegInf;          // running max in raw score units
         float l_run = 0.f;
 
-        // ---- prologue: NS-1 tiles in flight (Q, page ids and earlier stores drained first)
-        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_waitcnt(0);  // Q, ids and earlier stores drained
         #pragma unroll
         for (int k = 0; k < NS - 1; ++k)
             if (t_begin + k < t_end)
-                Issue::issue(p, b, g, L, ntp, t_begin + k, (t_begin + k) % NS, page_first, wave_u, lane);
+                ld.issue(p, b, g, L, ntp, t_begin + k, (t_begin + k) % NS, page_first, wave_u);
+        if (has_tree) build_ancestor_masks<NT>(p);   // overlaps the loads above
 
         for (int t = t_begin; t < t_end; ++t) {
             const int stage = t % NS;
@@ -347,121 +444,175 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                     if (last_page >= page_first + kPageCache) {
                         page_first = (tn * KT) >> p.p_shift;
                         wait_vmcnt<0>();
-                        load_page_window<NT>(p, b, page_first, npages);
+                        load_pages_and_parents<NT>(p, b, page_first, npages, true, false);
                     }
                 }
-                Issue::issue(p, b, g, L, ntp, tn, tn % NS, page_first, wave_u, lane);
+                ld.issue(p, b, g, L, ntp, tn, tn % NS, page_first, wave_u);
             }
 
-            const unsigned kbase = ring_base + stage * Gm::kStageBytes;
-            const unsigned vbase = kbase + Gm::kTileBytes;
+            const unsigned kaddr = ring_base + stage * Gm::kStageBytes + k_lane;
+            const unsigned vaddr = ring_base + stage * Gm::kStageBytes + Gm::kTileBytes + v_lane;
 
-            // The two 32-key halves of the tile are processed one after the other
-            // (scores, mask, softmax, PV) to bound register pressure.
+            // ---- scores of both 32-key halves: S^T[key][row] = K[key][:] . Q[row][:].
+            // At most 15 LDS reads can be tracked in flight; each half's K reads
+            // are issued while the previous MFMAs execute.
+            f32x16 s[2];
+            #pragma unroll
+            for (int hf = 0; hf < 2; ++hf)
+                #pragma unroll
+                for (int r = 0; r < 16; ++r) s[hf][r] = 0.f;
             #pragma unroll
             for (int hf = 0; hf < 2; ++hf) {
-                // S^T[key][row] = K[key][:] . Q[row][:], K fragments read in batches of 4
-                f32x16 s;
+                u32x4 kf[NKS];
                 #pragma unroll
-                for (int r = 0; r < 16; ++r) s[r] = 0.f;
-                // Row-aligned base of this lane's key row plus its swizzled chunk; the
-                // per-k-step chunk change only flips low-byte bits, so it is an XOR.
-                const unsigned kaddr0 = (kbase + col * Gm::kRowBytes) + ((half ^ (col % Gm::kChunks)) << 4);
+                for (int ks = 0; ks < NKS; ++ks)
+                    asm volatile("ds_read_b128 %0, %1 offset:%2"
+                                 : "=v"(kf[ks])
+                                 : "v"(kaddr ^ ((unsigned)ks << 5)), "i"(hf * 32 * Gm::kRowBytes));
+                constexpr int H = NKS / 2;
+                lds_wait<H>();
                 #pragma unroll
-                for (int kb4 = 0; kb4 < NKS / 4; ++kb4) {
-                    u32x4 kf[4];
-                    #pragma unroll
-                    for (int k4 = 0; k4 < 4; ++k4) {
-                        const int ks = kb4 * 4 + k4;
-                        asm volatile("ds_read_b128 %0, %1 offset:%2"
-                                     : "=v"(kf[k4])
-                                     : "v"(kaddr0 ^ ((unsigned)ks << 5)), "i"(hf * 32 * Gm::kRowBytes));
-                    }
-                    asm volatile("s_waitcnt lgkmcnt(0)"
-                                 : "+v"(kf[0]), "+v"(kf[1]), "+v"(kf[2]), "+v"(kf[3]));
-                    #pragma unroll
-                    for (int k4 = 0; k4 < 4; ++k4)
-                        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            __builtin_bit_cast(bf16x8, kf[k4]), qf[kb4 * 4 + k4], s, 0, 0, 0);
+                for (int ks = 0; ks < H; ++ks) {
+                    tie(kf[ks]);
+                    s[hf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, kf[ks]), qf[ks], s[hf], 0, 0, 0);
                 }
+                lds_wait<0>();
+                #pragma unroll
+                for (int ks = H; ks < NKS; ++ks) {
+                    tie(kf[ks]);
+                    s[hf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, kf[ks]), qf[ks], s[hf], 0, 0, 0);
+                }
+            }
+            // V fragments (transposing reads) of the first half; they arrive during
+            // the mask and softmax below
+            u32x2 vf[2][2][NDT][2];        // [half][kstep][dt][rr]
+            auto read_v = [&](int hf, int kstep) {
+                #pragma unroll
+                for (int dt = 0; dt < NDT; ++dt)
+                    #pragma unroll
+                    for (int rr = 0; rr < 2; ++rr) {
+                        const unsigned flip =
+                            (unsigned)((dt * 4) ^ swz<Gm::kChunks>((rr * 8) % Gm::kChunks)) << 4;
+                        const unsigned a = vaddr ^ flip;
+                        if (hf == 0 && kstep == 0)
+                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[0][0][dt][rr])
+                                         : "v"(a), "i"((rr * 8) * Gm::kRowBytes));
+                        else if (hf == 0)
+                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[0][1][dt][rr])
+                                         : "v"(a), "i"((16 + rr * 8) * Gm::kRowBytes));
+                        else if (kstep == 0)
+                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[1][0][dt][rr])
+                                         : "v"(a), "i"((32 + rr * 8) * Gm::kRowBytes));
+                        else
+                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[1][1][dt][rr])
+                                         : "v"(a), "i"((48 + rr * 8) * Gm::kRowBytes));
+                    }
+            };
+            read_v(0, 0);
+            read_v(0, 1);
 
-                // mask: lane holds keys hf*32 + (r/4)*8 + half*4 + r%4 of row `col`
-                if (t < ntp) {
-                    // keys >= lim are past the prefix; this lane's keys are kofs(r) + 4*half
-                    const int lim = L - t * KT - hf * 32 - half * 4;
-                    if (lim < 32) {
+            // ---- masks (only the tile that crosses the prefix end, and tree tiles).
+            // Lane holds keys hf*32 + (r/4)*8 + half*4 + r%4 of row `col`.
+            if (t < ntp) {
+                const int lim = L - t * KT - half * 4;          // keys >= lim are past the prefix
+                if (lim < 64) {
+                    #pragma unroll
+                    for (int hf = 0; hf < 2; ++hf)
                         #pragma unroll
                         for (int r = 0; r < 16; ++r)
-                            if ((r >> 2) * 8 + (r & 3) >= lim) s[r] = kNegInf;
-                    }
-                } else {
-                    const unsigned int vis =
-                        (unsigned int)(g_anc[node][t - ntp] >> (hf * 32 + half * 4));
+                            if (hf * 32 + (r >> 2) * 8 + (r & 3) >= lim) s[hf][r] = kNegInf;
+                }
+            } else {
+                const unsigned long long vis = g_anc[node][t - ntp] >> (half * 4);
+                #pragma unroll
+                for (int hf = 0; hf < 2; ++hf)
                     #pragma unroll
                     for (int r = 0; r < 16; ++r)
-                        if (!((vis >> ((r >> 2) * 8 + (r & 3))) & 1u)) s[r] = kNegInf;
-                }
+                        if (!((vis >> (hf * 32 + (r >> 2) * 8 + (r & 3))) & 1ull)) s[hf][r] = kNegInf;
+            }
 
-                // online softmax; the running max is only raised when a score exceeds
-                // it by more than kRescaleSlack (log2 units), so O is rarely rescaled
-                float tmax = s[0];
+            // ---- online softmax over the whole tile. The running max is only
+            // raised when a score exceeds it by more than kRescaleSlack (log2
+            // units), so O is rarely rescaled.
+            float tmax = fmaxf(s[0][0], s[1][0]);
+            #pragma unroll
+            for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, fmaxf(s[0][r], s[1][r]));
+            tmax = halves_max(tmax);
+            const bool raise = tmax * p.scale_log2 > m_run * p.scale_log2 + kRescaleSlack;
+            if (__any(raise)) {
+                const float m_new = raise ? tmax : m_run;
+                const float alpha = (m_run == kNegInf) ? 0.f
+                                    : __builtin_amdgcn_exp2f((m_run - m_new) * p.scale_log2);
+                l_run *= alpha;
                 #pragma unroll
-                for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, s[r]);
-                tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-                const bool raise = tmax * p.scale_log2 > m_run * p.scale_log2 + kRescaleSlack;
-                if (__any(raise)) {
-                    const float m_new = raise ? tmax : m_run;
-                    const float alpha = (m_run == kNegInf) ? 0.f
-                                        : __builtin_amdgcn_exp2f((m_run - m_new) * p.scale_log2);
-                    l_run *= alpha;
+                for (int dt = 0; dt < NDT; ++dt)
                     #pragma unroll
-                    for (int dt = 0; dt < NDT; ++dt)
-                        #pragma unroll
-                        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-                    m_run = m_new;
-                }
-                const float msc = (m_run == kNegInf) ? 0.f : m_run * p.scale_log2;
-                bf16x8 pb[2];
-                float psum = 0.f;
-                #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], p.scale_log2, -msc));
-                    psum += e;
-                    pb[r >> 3][r & 7] = (__bf16)e;
-                }
-                l_run += psum;
+                    for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+                m_run = m_new;
+            }
+            const float msc = (m_run == kNegInf) ? 0.f : m_run * p.scale_log2;
 
-                // O^T[d][row] += V^T[d][key] . P^T[key][row]; the key order inside each
-                // 16-key step matches the score layout on both operands.
-                // Supplying lane (j = lane % 16 of its group) names row j/4 of a 4-key
-                // block and 4 head-dim lanes; its swizzled chunk is (a ^ b) ^ const with
-                // a from the head-dim lane and b from the key, constants from (dt, rr).
-                const int va = ((lane >> 4) & 1) * 2 + ((lane & 3) >> 1);
-                const int vb = half * 4 + ((lane & 15) >> 2);
-                const unsigned vaddr0 = (vbase + vb * Gm::kRowBytes) + ((va ^ vb) << 4) + (lane & 1) * 8;
+            // P for the first half
+            bf16x8 pb[2][2];
+            float psum = 0.f;
+            #pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][r], p.scale_log2, -msc));
+                psum += e;
+                pb[0][r >> 3][r & 7] = (__bf16)e;
+            }
+            lds_wait<0>();                    // the first half's V fragments are in
+            #pragma unroll
+            for (int kstep = 0; kstep < 2; ++kstep)
                 #pragma unroll
-                for (int kstep = 0; kstep < 2; ++kstep)
-                    #pragma unroll
-                    for (int dt = 0; dt < NDT; ++dt) {
-                        u32x2 vf[2];
-                        #pragma unroll
-                        for (int rr = 0; rr < 2; ++rr) {
-                            const unsigned flip = (unsigned)((dt * 4) ^ ((rr * 8) % Gm::kChunks)) << 4;
-                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
-                                         : "=v"(vf[rr])
-                                         : "v"(vaddr0 ^ flip),
-                                           "i"((hf * 32 + kstep * 16 + rr * 8) * Gm::kRowBytes));
-                        }
-                        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(vf[0]), "+v"(vf[1]));
-                        const u32x4 a = {vf[0][0], vf[0][1], vf[1][0], vf[1][1]};
-                        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            __builtin_bit_cast(bf16x8, a), pb[kstep], o[dt], 0, 0, 0);
-                    }
+                for (int dt = 0; dt < NDT; ++dt) {
+                    tie(vf[0][kstep][dt][0]);
+                    tie(vf[0][kstep][dt][1]);
+                }
+            read_v(1, 0);
+            // PV of the first half interleaved with P of the second half
+            #pragma unroll
+            for (int kstep = 0; kstep < 2; ++kstep) {
+                if (kstep == 1) read_v(1, 1);
+                #pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    const u32x4 a = {vf[0][kstep][dt][0][0], vf[0][kstep][dt][0][1],
+                                     vf[0][kstep][dt][1][0], vf[0][kstep][dt][1][1]};
+                    o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, a), pb[0][kstep], o[dt], 0, 0, 0);
+                }
+            }
+            #pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1][r], p.scale_log2, -msc));
+                psum += e;
+                pb[1][r >> 3][r & 7] = (__bf16)e;
+            }
+            #pragma unroll
+            for (int i = 0; i < NDT; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+                __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // then VALU work
+            }
+            l_run += psum;
+            #pragma unroll
+            for (int kstep = 0; kstep < 2; ++kstep) {
+                if (kstep == 0) lds_wait<2 * NDT>(); else lds_wait<0>();
+                #pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    tie(vf[1][kstep][dt][0]);
+                    tie(vf[1][kstep][dt][1]);
+                    const u32x4 a = {vf[1][kstep][dt][0][0], vf[1][kstep][dt][0][1],
+                                     vf[1][kstep][dt][1][0], vf[1][kstep][dt][1][1]};
+                    o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, a), pb[1][kstep], o[dt], 0, 0, 0);
+                }
             }
         }
 
         // ---- finish the segment
-        const float l_tot = l_run + __shfl_xor(l_run, 32);
+        const float l_tot = halves_sum(l_run);
         if (complete) {
             if (row_ok) {
                 const float inv = 1.f / l_tot;

@@ -6,7 +6,7 @@
 #include <string.h>
 
 #define TREEVERIFY_BUILD 1
-#include "../../include/treeverify.h"
+#include "treeverify.h"
 #include "tv_internal.h"
 
 namespace {
@@ -183,6 +183,7 @@ int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
     p.max_pages = max_pages; p.num_pages = num_pages;
     p.rows_per_block = s.rows_per_block; p.row_blocks = s.row_blocks;
     p.tree_tiles_all_blocks = s.tree_tiles_all;
+    p.small_pages = P < 1024 / (2 * D) ? 1 : 0;
     p.num_wg = (int)num_wg;
     const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)D);
     p.scale = sc;

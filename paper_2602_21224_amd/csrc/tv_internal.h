@@ -31,6 +31,7 @@ struct AttnParams {
     int32_t *ws_cum;   // [B + 1] cumulative tile counts (written by workgroup 0)
     int B, N, Hq, Hkv, G, rows, P, p_shift, max_pages, num_pages;
     int rows_per_block, row_blocks;
+    int small_pages;             // pages shorter than one 1 KB load block of keys
     int tree_tiles_all_blocks;   // sum over row blocks of the tree tiles each needs
     int num_wg;
     float scale_log2;            // softmax scale * log2(e)
