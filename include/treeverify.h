@@ -113,8 +113,8 @@ TV_API const char *tv_status_string(int status);
  *               16-byte aligned; contents on entry do not matter; clobbered.
  *
  * Supported: D in {64, 128}; 1 <= N <= 256; Hq % Hkv == 0 and
- * (Hq / Hkv) * N <= 2048; 0 <= B <= 1024; P a power of two in [1, 256];
- * max_pages >= 1; num_pages >= 1.
+ * (Hq / Hkv) * N <= 2048; Hkv * D < 2^23; 0 <= B <= 1024; P a power of two
+ * in [1, 256]; max_pages >= 1; num_pages >= 1.
  * max_kv_len is a host-side upper bound of kv_len[] used only to size the
  * launch; results never depend on it (an understated bound costs speed only).
  * scale <= 0 selects 1/sqrt(D). q, k_tree, v_tree, k_cache, v_cache, out and

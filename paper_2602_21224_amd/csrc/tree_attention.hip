@@ -45,9 +45,10 @@ namespace {
 
 #define LDS_AS __attribute__((address_space(3)))
 #define GLOBAL_AS __attribute__((address_space(1)))
+#define CONST_AS __attribute__((address_space(4)))
 
 constexpr int KT = kKeyTile;           // 64 keys per tile
-constexpr int NS = 4;                  // ring stages
+constexpr int NS = 4;                  // ring stages (a power of two: stage = tile & (NS - 1))
 constexpr int kPageCache = 1024;       // page ids cached in LDS per segment window
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLn2 = 0.693147180559945309f;
@@ -260,93 +261,369 @@ __device__ void build_ancestor_masks(const AttnParams &p) {
     }
 }
 
-template <int D, int NW>
+template <int D, int NW, bool SMALL>
 struct TileIssue {
     using Gm = Geo<D>;
-    static constexpr int kLoadsPerWave = 2 * Gm::kBlocksPerTile / NW;
+    static constexpr int kLoadsPerWave = Gm::kBlocksPerTile / NW;   // per K (or V) tile
+    static constexpr int LPT = kLoadsPerWave;
     static constexpr int KPB = Gm::kKeysPerBlock;     // keys per 1 KB load block
     static constexpr int C = Gm::kChunks;
+    static_assert(LPT * NW == Gm::kBlocksPerTile, "blocks split evenly over waves");
+
+    // Wave-uniform addresses of this wave's load blocks of one tile: the K and
+    // V row of the block's first key, and how many of its KPB keys exist.
+    struct Blocks {
+        const char *k[LPT];
+        const char *v[LPT];
+        int nv[LPT];
+    };
 
     int kib;                                          // this lane's key within a block
     unsigned row_off;                                 // kib * key row stride (bytes)
-    unsigned chunk_off[kLoadsPerWave];                // swizzled chunk offset per load
+    unsigned chunk_off[LPT];                          // swizzled chunk offset per load
+    // per unit
+    const char *kc_g, *vc_g;                          // cache base + KV head g
+    const char *kt_g, *vt_g;                          // tree row of node 0, KV head g
+    unsigned row_bytes, page_bytes;                   // key row of all KV heads; one page
+    int L, ntp;
 
-    __device__ __forceinline__ void init(int wave_u, int lane, unsigned row_stride) {
+    __device__ __forceinline__ void init(int wave_u, int lane, const AttnParams &p) {
+        row_bytes = (unsigned)(p.Hkv * D * 2);
+        page_bytes = row_bytes << p.p_shift;
         kib = lane / C;
-        row_off = kib * row_stride;
+        row_off = kib * row_bytes;
         #pragma unroll
-        for (int i = 0; i < kLoadsPerWave; ++i) {
-            const int kb = (wave_u * kLoadsPerWave + i) % Gm::kBlocksPerTile;
+        for (int i = 0; i < LPT; ++i) {
+            const int kb = wave_u * LPT + i;
             chunk_off[i] = (unsigned)(((lane % C) ^ swz<C>((kb * KPB + kib) % C)) * 16);
         }
     }
 
-    // Issue the direct-to-LDS loads of tile t of unit (b, g) into ring stage
-    // `stage`. A load block covers KPB consecutive keys; when a page holds at
-    // least KPB keys they share one page, so the block's base address is
-    // wave-uniform (scalar math) and lanes only add their row/chunk offset.
-    // Rows that do not exist (past the prefix, past N) re-read the block's
-    // first row, or tree node 0 when the whole block is past the end.
-    __device__ __forceinline__ void issue(const AttnParams &p, int b, int g, int L, int ntp,
-                                          int t, int stage, int page_first, int wave_u) const {
-        const uint16_t *safe_k = p.k_tree + ((size_t)b * p.N * p.Hkv + g) * D;
-        const uint16_t *safe_v = p.v_tree + ((size_t)b * p.N * p.Hkv + g) * D;
+    __device__ __forceinline__ void set_unit(const AttnParams &p, int b, int g, int L_, int ntp_) {
+        L = L_;
+        ntp = ntp_;
+        kc_g = reinterpret_cast<const char *>(p.k_cache + (size_t)g * D);
+        vc_g = reinterpret_cast<const char *>(p.v_cache + (size_t)g * D);
+        kt_g = reinterpret_cast<const char *>(p.k_tree + ((size_t)b * p.N * p.Hkv + g) * D);
+        vt_g = reinterpret_cast<const char *>(p.v_tree + ((size_t)b * p.N * p.Hkv + g) * D);
+    }
+
+    // Page ids of this wave's load blocks of prefix tile t, by scalar loads
+    // through the constant address space: the ids land in SGPRs without
+    // touching LDS. The index is clamped into the table row, so the load is
+    // always in bounds; blocks() decides whether an id is used. Callers fetch
+    // one tile period before the loads are issued, and nothing here waits for
+    // the result.
+    __device__ __forceinline__ void fetch_pages(const AttnParams &p, int b, int t, int wave_u,
+                                                int (&pg)[LPT]) const {
+        const CONST_AS int32_t *row =
+            (const CONST_AS int32_t *)(p.page_table + (size_t)b * p.max_pages);
         #pragma unroll
-        for (int i = 0; i < kLoadsPerWave; ++i) {
-            const int blk = wave_u * kLoadsPerWave + i;                 // wave-uniform
-            const bool is_v = blk >= Gm::kBlocksPerTile;
-            const int kb = is_v ? blk - Gm::kBlocksPerTile : blk;
-            const uint16_t *base = is_v ? safe_v : safe_k;
-            const char *addr;
-            if (t < ntp) {
-                const int pos0 = t * KT + kb * KPB;
-                const int n_valid = min(max(L - pos0, 0), KPB);
-                if (!p.small_pages) {
-                    int pg = -1;
-                    if (n_valid > 0)
-                        pg = __builtin_amdgcn_readfirstlane(g_pages[(pos0 >> p.p_shift) - page_first]);
-                    const bool ok = pg >= 0;
-                    if (ok)
-                        base = (is_v ? p.v_cache : p.k_cache) +
-                               ((((size_t)pg << p.p_shift) + (pos0 & (p.P - 1))) * p.Hkv + g) * D;
-                    addr = reinterpret_cast<const char *>(base) +
-                           ((ok && kib < n_valid ? row_off : 0u) + chunk_off[i]);
-                } else {
-                    // pages shorter than a load block: every lane finds its own page
-                    const int pos = pos0 + kib;
-                    const uint16_t *row = base;
-                    if (kib < n_valid) {
-                        const int pg = g_pages[(pos >> p.p_shift) - page_first];
-                        if (pg >= 0)
-                            row = (is_v ? p.v_cache : p.k_cache) +
-                                  ((((size_t)pg << p.p_shift) + (pos & (p.P - 1))) * p.Hkv + g) * D;
-                    }
-                    addr = reinterpret_cast<const char *>(row) + chunk_off[i];
-                }
-            } else {
-                const int j0 = (t - ntp) * KT + kb * KPB;
-                const int n_valid = min(max(p.N - j0, 0), KPB);
-                if (n_valid > 0) base += (size_t)j0 * p.Hkv * D;
-                addr = reinterpret_cast<const char *>(base) + ((kib < n_valid ? row_off : 0u) + chunk_off[i]);
+        for (int i = 0; i < LPT; ++i) {
+            const int pos0 = t * KT + (wave_u * LPT + i) * KPB;
+            pg[i] = SMALL ? -1 : row[min(max(pos0 >> p.p_shift, 0), p.max_pages - 1)];
+        }
+    }
+
+    // Block addresses of tile t. A block with no existing row (past the prefix,
+    // past N, or with an invalid page id) points at tree node 0's row, which is
+    // always readable; its rows are masked later.
+    __device__ __forceinline__ Blocks blocks(const AttnParams &p, int t, int wave_u,
+                                             const int (&pg)[LPT]) const {
+        Blocks r;
+        if (t < ntp) {
+            const bool full = t * KT + KT <= L;            // every row of the tile exists
+            #pragma unroll
+            for (int i = 0; i < LPT; ++i) {
+                const int pos0 = t * KT + (wave_u * LPT + i) * KPB;
+                const bool ok = (unsigned)pg[i] < (unsigned)p.num_pages && (full || pos0 < L);
+                const size_t off = (size_t)(unsigned)pg[i] * (unsigned)page_bytes +
+                                   (unsigned)((pos0 & (p.P - 1)) * (unsigned)row_bytes);
+                r.k[i] = ok ? kc_g + off : kt_g;
+                r.v[i] = ok ? vc_g + off : vt_g;
+                r.nv[i] = !ok ? 0 : (full ? KPB : min(L - pos0, KPB));
             }
-            unsigned char *dst = g_ring + stage * Gm::kStageBytes + (is_v ? Gm::kTileBytes : 0) + kb * 1024;
-            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)addr, (LDS_AS void *)dst, 16, 0, 0);
+        } else {
+            #pragma unroll
+            for (int i = 0; i < LPT; ++i) {
+                const int j0 = (t - ntp) * KT + (wave_u * LPT + i) * KPB;
+                const int nv = min(max(p.N - j0, 0), KPB);
+                const unsigned off = nv > 0 ? (unsigned)j0 * (unsigned)row_bytes : 0u;
+                r.k[i] = kt_g + off;
+                r.v[i] = vt_g + off;
+                r.nv[i] = nv;
+            }
+        }
+        return r;
+    }
+
+    // Direct-to-LDS load of block i of this wave's share of one K (or V) tile
+    // into ring stage `stage`.
+    __device__ __forceinline__ void issue_one(const Blocks &bl, bool is_v, int stage, int wave_u,
+                                              int i) const {
+        unsigned char *dst = g_ring + stage * Gm::kStageBytes + (is_v ? Gm::kTileBytes : 0);
+        const char *addr = (is_v ? bl.v[i] : bl.k[i]) + ((kib < bl.nv[i] ? row_off : 0u) + chunk_off[i]);
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)addr,
+                                         (LDS_AS void *)(dst + (wave_u * LPT + i) * 1024), 16, 0, 0);
+    }
+
+    // Direct-to-LDS loads of this wave's blocks of one K (or V) tile into ring
+    // stage `stage`.
+    __device__ __forceinline__ void issue(const Blocks &bl, bool is_v, int stage, int wave_u) const {
+        unsigned char *dst = g_ring + stage * Gm::kStageBytes + (is_v ? Gm::kTileBytes : 0);
+        #pragma unroll
+        for (int i = 0; i < LPT; ++i) {
+            const char *addr = (is_v ? bl.v[i] : bl.k[i]) + ((kib < bl.nv[i] ? row_off : 0u) + chunk_off[i]);
+            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)addr,
+                                             (LDS_AS void *)(dst + (wave_u * LPT + i) * 1024), 16, 0, 0);
+        }
+    }
+
+    // Pages shorter than a load block: every lane looks up its own page in the
+    // LDS page-id window (prefix tiles only).
+    __device__ __forceinline__ void issue_small(const AttnParams &p, int t, bool is_v, int page_first,
+                                                int wave_u) const {
+        unsigned char *dst = g_ring + (t & (NS - 1)) * Gm::kStageBytes + (is_v ? Gm::kTileBytes : 0);
+        #pragma unroll
+        for (int i = 0; i < LPT; ++i) {
+            const int pos = t * KT + (wave_u * LPT + i) * KPB + kib;
+            const char *row = is_v ? vt_g : kt_g;
+            if (pos < L) {
+                const int id = g_pages[(pos >> p.p_shift) - page_first];
+                if (id >= 0)
+                    row = (is_v ? vc_g : kc_g) + (size_t)(unsigned)id * page_bytes + (size_t)(pos & (p.P - 1)) * row_bytes;
+            }
+            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(row + chunk_off[i]),
+                                             (LDS_AS void *)(dst + (wave_u * LPT + i) * 1024), 16, 0, 0);
         }
     }
 };
 
-template <int D, int NW>
+// Wait until at most n of this wave's vector-memory operations are still in
+// flight; a count without its own case waits for the next smaller one.
+__device__ __forceinline__ void wait_vm_at_most(int n) {
+    if (n >= 63) wait_vmcnt<63>();
+    else if (n >= 48) wait_vmcnt<48>();
+    else if (n >= 32) wait_vmcnt<32>();
+    else if (n >= 24) wait_vmcnt<24>();
+    else if (n >= 16) wait_vmcnt<16>();
+    else if (n >= 12) wait_vmcnt<12>();
+    else if (n >= 8) wait_vmcnt<8>();
+    else if (n >= 6) wait_vmcnt<6>();
+    else if (n >= 4) wait_vmcnt<4>();
+    else if (n >= 2) wait_vmcnt<2>();
+    else if (n >= 1) wait_vmcnt<1>();
+    else wait_vmcnt<0>();
+}
+
+// LDS-read wait with a count that is a constant once the caller is unrolled.
+__device__ __forceinline__ void lds_wait_n(int n) {
+    switch (n) {
+        case 0: lds_wait<0>(); break;
+        case 1: lds_wait<1>(); break;
+        case 2: lds_wait<2>(); break;
+        case 3: lds_wait<3>(); break;
+        case 4: lds_wait<4>(); break;
+        case 5: lds_wait<5>(); break;
+        case 6: lds_wait<6>(); break;
+        case 7: lds_wait<7>(); break;
+        case 8: lds_wait<8>(); break;
+        default: lds_wait<0>(); break;
+    }
+}
+
+// Per-wave state of one segment: Q fragments (MFMA B operand), O^T
+// accumulators, the current tile's scores and probabilities, running max/sum.
+template <int D>
+struct WaveState {
+    static constexpr int NKS = D / 16;     // MFMA k-steps over the head dim
+    static constexpr int NDT = D / 32;     // 32-wide head-dim tiles of the output
+    bf16x8 qf[NKS];
+    f32x16 o[NDT];
+    f32x16 s[2];                           // S^T of the 2 x 32 keys of the tile
+    bf16x8 pb[4];                          // P^T, 16 keys per k-step
+    float m_run;                           // running max (raw score units)
+    float l_run;                           // this lane's part of the running sum
+};
+
+// Matrix phase of one wave: O^T += V^T P^T for the previous tile (PV) and
+// S^T = K Q^T for the current tile (SC). The ring reads are issued two
+// groups ahead of the MFMAs that consume them; groups alternate PV / S so
+// that consecutive MFMAs rarely depend on each other. hook(g) runs after
+// group g: the caller issues its global->LDS tile loads there, a few at a
+// time, instead of in one burst that would stall the wave.
+template <int D, bool PV, bool SC, typename Hook>
+__device__ __forceinline__ void matrix_phase(WaveState<D> &st, unsigned kaddr, unsigned vaddr,
+                                             Hook &&hook) {
+    using Gm = Geo<D>;
+    constexpr int NKS = D / 16, NDT = D / 32, KH = NKS / 2;
+    constexpr int C = Gm::kChunks;
+    // group g: even g = PV k-step g/2, odd g = S quarter g/2 (half q/2, k-range q%2)
+    constexpr int kGroups = 8;
+    auto active = [](int gi) { return (gi & 1) ? SC : PV; };
+    auto reads_of = [](int gi) { return (gi & 1) ? KH : 2 * NDT; };
+    u32x2 vb[4][NDT][2];
+    u32x4 kb[4][KH];
+    auto issue = [&](int gi) {
+        if (gi & 1) {
+            const int q = gi >> 1, hf = q >> 1, part = q & 1;
+            #pragma unroll
+            for (int i = 0; i < KH; ++i) {
+                const int ks = part * KH + i;
+                asm volatile("ds_read_b128 %0, %1 offset:%2"
+                             : "=v"(kb[q][i])
+                             : "v"(kaddr ^ ((unsigned)ks << 5)), "i"(hf * 32 * Gm::kRowBytes));
+            }
+        } else {
+            const int kk = gi >> 1;
+            #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+                #pragma unroll
+                for (int rr = 0; rr < 2; ++rr) {
+                    const unsigned flip = (unsigned)((dt * 4) ^ swz<C>((rr * 8) % C)) << 4;
+                    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                                 : "=v"(vb[kk][dt][rr])
+                                 : "v"(vaddr ^ flip), "i"((kk * 16 + rr * 8) * Gm::kRowBytes));
+                }
+        }
+    };
+    auto consume = [&](int gi) {
+        if (gi & 1) {
+            const int q = gi >> 1, hf = q >> 1, part = q & 1;
+            #pragma unroll
+            for (int i = 0; i < KH; ++i) {
+                tie(kb[q][i]);
+                st.s[hf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, kb[q][i]), st.qf[part * KH + i], st.s[hf], 0, 0, 0);
+            }
+        } else {
+            const int kk = gi >> 1;
+            #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                tie(vb[kk][dt][0]);
+                tie(vb[kk][dt][1]);
+                const u32x4 a = {vb[kk][dt][0][0], vb[kk][dt][0][1], vb[kk][dt][1][0], vb[kk][dt][1][1]};
+                st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, a), st.pb[kk], st.o[dt], 0, 0, 0);
+            }
+        }
+    };
+    if (SC) {
+        #pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+            #pragma unroll
+            for (int r = 0; r < 16; ++r) st.s[hf][r] = 0.f;
+    }
+    // active groups in order; next(gi) = following active group (or kGroups)
+    auto next = [&](int gi) {
+        int n = gi + 1;
+        while (n < kGroups && !active(n)) ++n;
+        return n;
+    };
+    const int g0 = next(-1);
+    const int g1 = next(g0);
+    issue(g0);
+    if (g1 < kGroups) issue(g1);
+    #pragma unroll
+    for (int gi = 0; gi < kGroups; ++gi) {
+        if (active(gi)) {
+            const int gn = next(gi);
+            lds_wait_n(gn < kGroups ? reads_of(gn) : 0);
+            consume(gi);
+            const int gnn = gn < kGroups ? next(gn) : kGroups;
+            if (gnn < kGroups) issue(gnn);
+        }
+        hook(gi);          // the caller's tile loads, spread over the phase
+    }
+}
+
+// Softmax phase of one wave for tile t: mask, tile max, lazy rescale of the
+// running state, exponentials into P^T (bf16) and the running sum.
+template <int D>
+__device__ __forceinline__ void softmax_phase(WaveState<D> &st, const AttnParams &p, int t,
+                                              int ntp, int L, int node, int half) {
+    constexpr int NDT = D / 32;
+    // Lane holds keys hf*32 + (r/4)*8 + half*4 + r%4 of its row.
+    if (t < ntp) {
+        const int lim_t = L - t * KT;                   // keys >= lim_t are past the prefix
+        if (lim_t < KT) {                               // wave-uniform: only the last prefix tile
+            const int lim = lim_t - half * 4;
+            #pragma unroll
+            for (int hf = 0; hf < 2; ++hf)
+                #pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    st.s[hf][r] = (hf * 32 + (r >> 2) * 8 + (r & 3) >= lim) ? kNegInf : st.s[hf][r];
+        }
+    } else {
+        const unsigned long long vis = g_anc[node][t - ntp] >> (half * 4);
+        #pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+            #pragma unroll
+            for (int r = 0; r < 16; ++r)
+                st.s[hf][r] = ((vis >> (hf * 32 + (r >> 2) * 8 + (r & 3))) & 1ull) ? st.s[hf][r] : kNegInf;
+    }
+    // The running max is only raised when a score exceeds it by more than
+    // kRescaleSlack (log2 units), so O is rarely rescaled. Reductions are
+    // trees so that the dependent chains stay short.
+    float mx[16];
+    #pragma unroll
+    for (int r = 0; r < 16; ++r) mx[r] = fmaxf(st.s[0][r], st.s[1][r]);
+    #pragma unroll
+    for (int w = 8; w >= 1; w >>= 1)
+        #pragma unroll
+        for (int r = 0; r < w; ++r) mx[r] = fmaxf(mx[r], mx[r + w]);
+    const float tmax = halves_max(mx[0]);
+    const bool raise = tmax * p.scale_log2 > st.m_run * p.scale_log2 + kRescaleSlack;
+    if (__any(raise)) {
+        const float m_new = raise ? tmax : st.m_run;
+        const float alpha = (st.m_run == kNegInf) ? 0.f
+                            : __builtin_amdgcn_exp2f((st.m_run - m_new) * p.scale_log2);
+        st.l_run *= alpha;
+        #pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+            #pragma unroll
+            for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
+        st.m_run = m_new;
+    }
+    const float msc = (st.m_run == kNegInf) ? 0.f : st.m_run * p.scale_log2;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+        #pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float x = __builtin_amdgcn_exp2f(
+                __builtin_fmaf(st.s[kk >> 1][(kk & 1) * 8 + e], p.scale_log2, -msc));
+            ps[e & 3] += x;
+            st.pb[kk][e] = (__bf16)x;
+        }
+    const float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
+    st.l_run += psum;
+}
+
+// Barrier between the phases of the two wave groups; nothing is scheduled
+// across it.
+__device__ __forceinline__ void phase_barrier() {
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int D, int NW, bool SMALL>
 __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p) {
     using Gm = Geo<D>;
-    using Issue = TileIssue<D, NW>;
+    using Issue = TileIssue<D, NW, SMALL>;
     constexpr int NT = NW * kWave;
-    constexpr int NKS = D / 16;     // MFMA k-steps over the head dim
-    constexpr int NDT = D / 32;     // 32-wide head-dim tiles of the output
-    constexpr int LPW = Issue::kLoadsPerWave;
+    constexpr int NKS = D / 16;
+    constexpr int NDT = D / 32;
+    constexpr int LPT = Issue::kLoadsPerWave;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave_u = __builtin_amdgcn_readfirstlane(tid / kWave);
+    // Two wave groups run half a tile apart: while one group is in its matrix
+    // phase the other is in its softmax phase, so every SIMD has MFMA and VALU
+    // work from different waves at the same time.
+    const int grp = (NW >= 2 && wave_u >= NW / 2) ? 1 : 0;
     const int half = lane >> 5;
     const int col = lane & 31;
     const int w = xcd_contiguous_id(blockIdx.x, p.num_wg);
@@ -361,7 +638,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
     const int end = min(start + share, total);
     const unsigned ring_base = lds_addr(g_ring);
     Issue ld;
-    ld.init(wave_u, lane, (unsigned)(p.Hkv * D * 2));
+    ld.init(wave_u, lane, p);
 
     // lane-constant parts of the LDS fragment addresses (see swz)
     const unsigned k_lane = col * Gm::kRowBytes + ((half ^ swz<Gm::kChunks>(col % Gm::kChunks)) << 4);
@@ -392,227 +669,197 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             ++rb;
             ulen = ntp + tree_tiles_of_block(rb, p);
         }
-        const int t_begin = off;
+        const int t0 = off;
         const int t_end = min(ulen, off + (end - pos));
-        const bool complete = (t_begin == 0 && t_end == ulen);
+        const bool complete = (t0 == 0 && t_end == ulen);
 
         // ---- this wave's 32 query rows: Q fragments stay in registers
         const int row = rb * p.rows_per_block + wave_u * kRowsPerWave + col;
         const bool row_ok = row < p.rows;
         const int node = row_ok ? row / p.G : 0;
         const int hq = g * p.G + (row_ok ? row % p.G : 0);
-        bf16x8 qf[NKS];
+        WaveState<D> st;
         {
             const uint16_t *qp = p.q + (((size_t)b * p.N + node) * p.Hq + hq) * D + half * 8;
             #pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
                 u16x8 v = row_ok ? *reinterpret_cast<const u16x8 *>(qp + ks * 16)
                                  : u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-                qf[ks] = __builtin_bit_cast(bf16x8, v);
+                st.qf[ks] = __builtin_bit_cast(bf16x8, v);
             }
         }
-
-        // ---- page ids and parent links (one round trip), then the first tiles
-        const int npages = (L + p.P - 1) >> p.p_shift;
-        int page_first = (t_begin * KT) >> p.p_shift;
-        const bool has_tree = t_end > ntp;
-        load_pages_and_parents<NT>(p, b, page_first, npages, t_begin < ntp, has_tree);
-
-        f32x16 o[NDT];
         #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
             #pragma unroll
-            for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
-        float m_run = kNegInf;          // running max in raw score units
-        float l_run = 0.f;
+            for (int r = 0; r < 16; ++r) st.o[dt][r] = 0.f;
+        st.m_run = kNegInf;
+        st.l_run = 0.f;
 
-        __builtin_amdgcn_s_waitcnt(0);  // Q, ids and earlier stores drained
-        #pragma unroll
-        for (int k = 0; k < NS - 1; ++k)
-            if (t_begin + k < t_end)
-                ld.issue(p, b, g, L, ntp, t_begin + k, (t_begin + k) % NS, page_first, wave_u);
-        if (has_tree) build_ancestor_masks<NT>(p);   // overlaps the loads above
+        const int npages = (L + p.P - 1) >> p.p_shift;
+        const bool has_tree = t_end > ntp;
+        auto kaddr_of = [&](int t) { return ring_base + (t & (NS - 1)) * Gm::kStageBytes + k_lane; };
+        auto vaddr_of = [&](int t) {
+            return ring_base + (t & (NS - 1)) * Gm::kStageBytes + Gm::kTileBytes + v_lane;
+        };
 
-        for (int t = t_begin; t < t_end; ++t) {
-            const int stage = t % NS;
-            wait_tile_loads(min(NS - 2, t_end - 1 - t), LPW);
-            lds_barrier();
-            const int tn = t + NS - 1;
-            if (tn < t_end) {
-                if (tn < ntp) {
-                    const int last_page = (min(tn * KT + KT, L) - 1) >> p.p_shift;
-                    if (last_page >= page_first + kPageCache) {
-                        page_first = (tn * KT) >> p.p_shift;
-                        wait_vmcnt<0>();
-                        load_pages_and_parents<NT>(p, b, page_first, npages, true, false);
-                    }
-                }
-                ld.issue(p, b, g, L, ntp, tn, tn % NS, page_first, wave_u);
+        // The segment runs in sub-ranges whose prefix pages fit the LDS page-id
+        // window (one sub-range unless a piece spans more than kPageCache pages).
+        for (int ta = t0; ta < t_end;) {
+            const int page_first = (ta * KT) >> p.p_shift;
+            int tb = t_end;
+            if (ta < ntp) {
+                const int t_cov = ((page_first + kPageCache) << p.p_shift) / KT;   // first tile not covered
+                if (t_cov < ntp) tb = min(tb, t_cov);
             }
+            const bool first = (ta == t0);
+            load_pages_and_parents<NT>(p, b, page_first, npages, ta < ntp, first && has_tree);
 
-            const unsigned kaddr = ring_base + stage * Gm::kStageBytes + k_lane;
-            const unsigned vaddr = ring_base + stage * Gm::kStageBytes + Gm::kTileBytes + v_lane;
-
-            // ---- scores of both 32-key halves: S^T[key][row] = K[key][:] . Q[row][:].
-            // At most 15 LDS reads can be tracked in flight; each half's K reads
-            // are issued while the previous MFMAs execute.
-            f32x16 s[2];
-            #pragma unroll
-            for (int hf = 0; hf < 2; ++hf)
-                #pragma unroll
-                for (int r = 0; r < 16; ++r) s[hf][r] = 0.f;
-            #pragma unroll
-            for (int hf = 0; hf < 2; ++hf) {
-                u32x4 kf[NKS];
-                #pragma unroll
-                for (int ks = 0; ks < NKS; ++ks)
-                    asm volatile("ds_read_b128 %0, %1 offset:%2"
-                                 : "=v"(kf[ks])
-                                 : "v"(kaddr ^ ((unsigned)ks << 5)), "i"(hf * 32 * Gm::kRowBytes));
-                constexpr int H = NKS / 2;
-                lds_wait<H>();
-                #pragma unroll
-                for (int ks = 0; ks < H; ++ks) {
-                    tie(kf[ks]);
-                    s[hf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, kf[ks]), qf[ks], s[hf], 0, 0, 0);
-                }
-                lds_wait<0>();
-                #pragma unroll
-                for (int ks = H; ks < NKS; ++ks) {
-                    tie(kf[ks]);
-                    s[hf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, kf[ks]), qf[ks], s[hf], 0, 0, 0);
-                }
-            }
-            // V fragments (transposing reads) of the first half; they arrive during
-            // the mask and softmax below
-            u32x2 vf[2][2][NDT][2];        // [half][kstep][dt][rr]
-            auto read_v = [&](int hf, int kstep) {
-                #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt)
-                    #pragma unroll
-                    for (int rr = 0; rr < 2; ++rr) {
-                        const unsigned flip =
-                            (unsigned)((dt * 4) ^ swz<Gm::kChunks>((rr * 8) % Gm::kChunks)) << 4;
-                        const unsigned a = vaddr ^ flip;
-                        if (hf == 0 && kstep == 0)
-                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[0][0][dt][rr])
-                                         : "v"(a), "i"((rr * 8) * Gm::kRowBytes));
-                        else if (hf == 0)
-                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[0][1][dt][rr])
-                                         : "v"(a), "i"((16 + rr * 8) * Gm::kRowBytes));
-                        else if (kstep == 0)
-                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[1][0][dt][rr])
-                                         : "v"(a), "i"((32 + rr * 8) * Gm::kRowBytes));
-                        else
-                            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(vf[1][1][dt][rr])
-                                         : "v"(a), "i"((48 + rr * 8) * Gm::kRowBytes));
-                    }
+            const int T = tb - ta;
+            // Load batch i = K tile ta+i and V tile ta+i-1 (those that exist). It is
+            // issued three tile periods before the matrix phase that first needs it.
+            auto batch_loads = [&](int i) {
+                return ((i >= 0 && i < T) ? LPT : 0) + ((i >= 1 && i <= T) ? LPT : 0);
             };
-            read_v(0, 0);
-            read_v(0, 1);
+            // pk: page ids of the K tile of the next batch (fetched one tile
+            // period ahead); last: blocks of the last issued K tile, which is
+            // the V tile of the next batch.
+            int pk[LPT];
+            typename Issue::Blocks last;
+            auto issue_batch = [&](int i) {
+                const int tk = ta + i, tv = ta + i - 1;
+                if (SMALL) {
+                    if (i < T) {
+                        if (tk < ntp) ld.issue_small(p, tk, false, page_first, wave_u);
+                        else ld.issue(ld.blocks(p, tk, wave_u, pk), false, tk & (NS - 1), wave_u);
+                    }
+                    if (i >= 1 && i <= T) {
+                        if (tv < ntp) ld.issue_small(p, tv, true, page_first, wave_u);
+                        else ld.issue(ld.blocks(p, tv, wave_u, pk), true, tv & (NS - 1), wave_u);
+                    }
+                    return;
+                }
+                typename Issue::Blocks cur;
+                if (i < T) {
+                    cur = ld.blocks(p, tk, wave_u, pk);
+                    ld.issue(cur, false, tk & (NS - 1), wave_u);
+                }
+                if (i >= 1 && i <= T) ld.issue(last, true, tv & (NS - 1), wave_u);
+                last = cur;
+            };
+            auto fetch = [&](int i) { ld.fetch_pages(p, b, ta + i, wave_u, pk); };
 
-            // ---- masks (only the tile that crosses the prefix end, and tree tiles).
-            // Lane holds keys hf*32 + (r/4)*8 + half*4 + r%4 of row `col`.
-            if (t < ntp) {
-                const int lim = L - t * KT - half * 4;          // keys >= lim are past the prefix
-                if (lim < 64) {
-                    #pragma unroll
-                    for (int hf = 0; hf < 2; ++hf)
-                        #pragma unroll
-                        for (int r = 0; r < 16; ++r)
-                            if (hf * 32 + (r >> 2) * 8 + (r & 3) >= lim) s[hf][r] = kNegInf;
-                }
-            } else {
-                const unsigned long long vis = g_anc[node][t - ntp] >> (half * 4);
-                #pragma unroll
-                for (int hf = 0; hf < 2; ++hf)
-                    #pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        if (!((vis >> (hf * 32 + (r >> 2) * 8 + (r & 3))) & 1ull)) s[hf][r] = kNegInf;
-            }
+            __builtin_amdgcn_s_waitcnt(0);  // Q, ids and earlier stores drained
+            ld.set_unit(p, b, g, L, ntp);
+            fetch(0);
+            issue_batch(0);
+            fetch(1);
+            issue_batch(1);
+            fetch(2);
+            issue_batch(2);
+            fetch(3);
+            if (first && has_tree) build_ancestor_masks<NT>(p);   // overlaps the loads above
 
-            // ---- online softmax over the whole tile. The running max is only
-            // raised when a score exceeds it by more than kRescaleSlack (log2
-            // units), so O is rarely rescaled.
-            float tmax = fmaxf(s[0][0], s[1][0]);
-            #pragma unroll
-            for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, fmaxf(s[0][r], s[1][r]));
-            tmax = halves_max(tmax);
-            const bool raise = tmax * p.scale_log2 > m_run * p.scale_log2 + kRescaleSlack;
-            if (__any(raise)) {
-                const float m_new = raise ? tmax : m_run;
-                const float alpha = (m_run == kNegInf) ? 0.f
-                                    : __builtin_amdgcn_exp2f((m_run - m_new) * p.scale_log2);
-                l_run *= alpha;
-                #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt)
-                    #pragma unroll
-                    for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-                m_run = m_new;
+            // Slots of half a tile period, separated by workgroup barriers. Group 0
+            // runs matrix j in slot 2j and softmax j in slot 2j+1; group 1 runs
+            // the same instruction stream one slot later (one extra barrier at
+            // its start, one at group 0's end). Batch j must have landed, for
+            // every wave, before slot 2j: group 0 waits before the barrier that
+            // opens its matrix j, group 1 before the one that opens its softmax
+            // j-1. Both groups issue batch j+3 when they start matrix j; the
+            // ring stages it overwrites were last read in slot 2j-1.
+            if (grp == 1) {
+                wait_vm_at_most(batch_loads(1) + batch_loads(2));
+                phase_barrier();
             }
-            const float msc = (m_run == kNegInf) ? 0.f : m_run * p.scale_log2;
-
-            // P for the first half
-            bf16x8 pb[2][2];
-            float psum = 0.f;
-            #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][r], p.scale_log2, -msc));
-                psum += e;
-                pb[0][r >> 3][r & 7] = (__bf16)e;
-            }
-            lds_wait<0>();                    // the first half's V fragments are in
-            #pragma unroll
-            for (int kstep = 0; kstep < 2; ++kstep)
-                #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    tie(vf[0][kstep][dt][0]);
-                    tie(vf[0][kstep][dt][1]);
+            // slot pair j: barrier, matrix j (issuing batch j+3 along the way);
+            // barrier, softmax j
+            typename Issue::Blocks cur;
+            bool have_k = false, have_v = false;
+            int stage_k = 0, stage_v = 0;
+            // Waits: batch j (group 0, before matrix j) or batch j+1 (group 1,
+            // before softmax j) complete; while the two later batches are full,
+            // that leaves 4 * LPT loads in flight, otherwise wait for all.
+            auto open_matrix = [&](int j) {
+                if (grp == 0) {
+                    if (j + 3 <= T) wait_vmcnt<4 * LPT < 63 ? 4 * LPT : 63>();
+                    else wait_vmcnt<0>();
                 }
-            read_v(1, 0);
-            // PV of the first half interleaved with P of the second half
-            #pragma unroll
-            for (int kstep = 0; kstep < 2; ++kstep) {
-                if (kstep == 1) read_v(1, 1);
-                #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    const u32x4 a = {vf[0][kstep][dt][0][0], vf[0][kstep][dt][0][1],
-                                     vf[0][kstep][dt][1][0], vf[0][kstep][dt][1][1]};
-                    o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, a), pb[0][kstep], o[dt], 0, 0, 0);
+                phase_barrier();
+                const int i = j + 3;
+                have_k = have_v = false;
+                if (i <= T) {
+                    if (SMALL) {
+                        issue_batch(i);
+                    } else {
+                        have_k = i < T;
+                        have_v = true;
+                        stage_k = (ta + i) & (NS - 1);
+                        stage_v = (ta + i - 1) & (NS - 1);
+                        if (have_k) cur = ld.blocks(p, ta + i, wave_u, pk);
+                    }
                 }
-            }
-            #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1][r], p.scale_log2, -msc));
-                psum += e;
-                pb[1][r >> 3][r & 7] = (__bf16)e;
-            }
-            #pragma unroll
-            for (int i = 0; i < NDT; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-                __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // then VALU work
-            }
-            l_run += psum;
-            #pragma unroll
-            for (int kstep = 0; kstep < 2; ++kstep) {
-                if (kstep == 0) lds_wait<2 * NDT>(); else lds_wait<0>();
+            };
+            // Loads of batch j+3 during matrix j: full batches in the steady
+            // state, the tail checks which halves exist.
+            auto hook_full = [&](int gi) {
+                if (SMALL) return;
                 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    tie(vf[1][kstep][dt][0]);
-                    tie(vf[1][kstep][dt][1]);
-                    const u32x4 a = {vf[1][kstep][dt][0][0], vf[1][kstep][dt][0][1],
-                                     vf[1][kstep][dt][1][0], vf[1][kstep][dt][1][1]};
-                    o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, a), pb[1][kstep], o[dt], 0, 0, 0);
+                for (int k = 0; k < 2 * LPT; ++k) {
+                    if (k * 8 / (2 * LPT) != gi) continue;
+                    if (k < LPT) ld.issue_one(cur, false, stage_k, wave_u, k);
+                    else ld.issue_one(last, true, stage_v, wave_u, k - LPT);
                 }
+            };
+            auto hook = [&](int gi) {
+                if (SMALL) return;
+                #pragma unroll
+                for (int k = 0; k < 2 * LPT; ++k) {
+                    if (k * 8 / (2 * LPT) != gi) continue;
+                    if (k < LPT) {
+                        if (have_k) ld.issue_one(cur, false, stage_k, wave_u, k);
+                    } else if (have_v) {
+                        ld.issue_one(last, true, stage_v, wave_u, k - LPT);
+                    }
+                }
+            };
+            auto close_matrix = [&]() {
+                if (!SMALL && have_v) last = cur;
+            };
+            auto softmax = [&](int j) {
+                if (grp == 1) {
+                    if (j + 4 <= T) wait_vmcnt<4 * LPT < 63 ? 4 * LPT : 63>();
+                    else wait_vmcnt<0>();
+                }
+                phase_barrier();
+                softmax_phase<D>(st, p, ta + j, ntp, L, node, half);
+                fetch(j + 4);          // ids for the batch issued at the next matrix phase
+            };
+            open_matrix(0);
+            matrix_phase<D, false, true>(st, kaddr_of(ta), 0u, hook);
+            close_matrix();
+            softmax(0);
+            int j = 1;
+            for (; j + 3 < T; ++j) {                 // batch j+3 is full
+                open_matrix(j);
+                matrix_phase<D, true, true>(st, kaddr_of(ta + j), vaddr_of(ta + j - 1), hook_full);
+                close_matrix();
+                softmax(j);
             }
+            for (; j < T; ++j) {
+                open_matrix(j);
+                matrix_phase<D, true, true>(st, kaddr_of(ta + j), vaddr_of(ta + j - 1), hook);
+                close_matrix();
+                softmax(j);
+            }
+            open_matrix(T);
+            matrix_phase<D, true, false>(st, 0u, vaddr_of(ta + T - 1), hook);
+            if (grp == 0 && NW >= 2) phase_barrier();
+            ta = tb;
+            __syncthreads();               // ring and page ids are reused next
         }
 
         // ---- finish the segment
-        const float l_tot = halves_sum(l_run);
+        const float l_tot = halves_sum(st.l_run);
         if (complete) {
             if (row_ok) {
                 const float inv = 1.f / l_tot;
@@ -623,12 +870,12 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                     for (int q4 = 0; q4 < 4; ++q4) {
                         bf16x4 v;
                         #pragma unroll
-                        for (int i = 0; i < 4; ++i) v[i] = (__bf16)(o[dt][q4 * 4 + i] * inv);
+                        for (int i = 0; i < 4; ++i) v[i] = (__bf16)(st.o[dt][q4 * 4 + i] * inv);
                         *reinterpret_cast<bf16x4 *>(op + dt * 32 + q4 * 8 + half * 4) = v;
                     }
                 if (p.lse && half == 0)
                     p.lse[((size_t)b * p.N + node) * p.Hq + hq] =
-                        m_run * p.scale + __builtin_amdgcn_logf(l_tot) * kLn2;
+                        st.m_run * p.scale + __builtin_amdgcn_logf(l_tot) * kLn2;
             }
         } else {
             const int slot = w * 2 + (seg_no == 0 ? 0 : 1);
@@ -638,18 +885,18 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             for (int dt = 0; dt < NDT; ++dt)
                 #pragma unroll
                 for (int q4 = 0; q4 < 4; ++q4) {
-                    f32x4 v = {o[dt][q4 * 4 + 0], o[dt][q4 * 4 + 1], o[dt][q4 * 4 + 2], o[dt][q4 * 4 + 3]};
+                    f32x4 v = {st.o[dt][q4 * 4 + 0], st.o[dt][q4 * 4 + 1], st.o[dt][q4 * 4 + 2],
+                               st.o[dt][q4 * 4 + 3]};
                     *reinterpret_cast<f32x4 *>(po + dt * 32 + q4 * 8 + half * 4) = v;
                 }
             if (half == 0) {
                 float *pm = p.ws_ml + ((size_t)slot * p.rows_per_block + rloc) * 2;
-                pm[0] = (m_run == kNegInf) ? kNegInf : m_run * p.scale_log2;
+                pm[0] = (st.m_run == kNegInf) ? kNegInf : st.m_run * p.scale_log2;
                 pm[1] = l_tot;
             }
         }
-        pos += t_end - t_begin;
+        pos += t_end - t0;
         ++seg_no;
-        __syncthreads();
     }
 }
 
@@ -710,7 +957,10 @@ __global__ __launch_bounds__(256) void tree_attention_merge_kernel(AttnParams p)
 
 template <int D, int NW>
 hipError_t launch_dn(const AttnParams &p, hipStream_t s) {
-    hipLaunchKernelGGL((tree_attention_kernel<D, NW>), dim3(p.num_wg), dim3(NW * kWave), 0, s, p);
+    if (p.small_pages)
+        hipLaunchKernelGGL((tree_attention_kernel<D, NW, true>), dim3(p.num_wg), dim3(NW * kWave), 0, s, p);
+    else
+        hipLaunchKernelGGL((tree_attention_kernel<D, NW, false>), dim3(p.num_wg), dim3(NW * kWave), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (p.num_wg > 1) {

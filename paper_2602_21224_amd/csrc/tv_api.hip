@@ -90,6 +90,9 @@ bool attn_shape_ok(int B, int N, int Hq, int Hkv, int D) {
     if (D != 64 && D != 128) return false;
     if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return false;
     if ((long)(Hq / Hkv) * N > 2048) return false;
+    // 256 key rows of all KV heads (a page, or the tree's rows) stay below 4 GiB,
+    // so in-kernel row offsets fit 32 bits
+    if ((long)Hkv * D * 2 * 256 >= (1l << 32)) return false;
     return true;
 }
 
