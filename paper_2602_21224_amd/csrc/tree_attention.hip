@@ -85,6 +85,12 @@ __device__ __forceinline__ float halves_max(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
+// Maximum of three values in one instruction (scores are never signalling NaNs).
+__device__ __forceinline__ float max3(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
 __device__ __forceinline__ float halves_sum(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
@@ -333,12 +339,13 @@ struct TileIssue {
         Blocks r;
         if (t < ntp) {
             const bool full = t * KT + KT <= L;            // every row of the tile exists
+            const int pos_w = t * KT + wave_u * LPT * KPB;  // first key of this wave's blocks
             #pragma unroll
             for (int i = 0; i < LPT; ++i) {
-                const int pos0 = t * KT + (wave_u * LPT + i) * KPB;
+                const int pos0 = pos_w + i * KPB;
                 const bool ok = (unsigned)pg[i] < (unsigned)p.num_pages && (full || pos0 < L);
-                const size_t off = (size_t)(unsigned)pg[i] * (unsigned)page_bytes +
-                                   (unsigned)((pos0 & (p.P - 1)) * (unsigned)row_bytes);
+                const size_t off = (size_t)(unsigned)pg[i] * page_bytes +
+                                   (unsigned)((pos0 & (p.P - 1)) * row_bytes);
                 r.k[i] = ok ? kc_g + off : kt_g;
                 r.v[i] = ok ? vc_g + off : vt_g;
                 r.nv[i] = !ok ? 0 : (full ? KPB : min(L - pos0, KPB));
@@ -563,16 +570,22 @@ __device__ __forceinline__ void softmax_phase(WaveState<D> &st, const AttnParams
                 st.s[hf][r] = ((vis >> (hf * 32 + (r >> 2) * 8 + (r & 3))) & 1ull) ? st.s[hf][r] : kNegInf;
     }
     // The running max is only raised when a score exceeds it by more than
-    // kRescaleSlack (log2 units), so O is rarely rescaled. Reductions are
-    // trees so that the dependent chains stay short.
-    float mx[16];
+    // kRescaleSlack (log2 units), so O is rarely rescaled. The tile max is a
+    // tree of three-input maxes.
+    float v[32];
     #pragma unroll
-    for (int r = 0; r < 16; ++r) mx[r] = fmaxf(st.s[0][r], st.s[1][r]);
+    for (int r = 0; r < 16; ++r) {
+        v[r] = st.s[0][r];
+        v[16 + r] = st.s[1][r];
+    }
+    float m1[12];
     #pragma unroll
-    for (int w = 8; w >= 1; w >>= 1)
-        #pragma unroll
-        for (int r = 0; r < w; ++r) mx[r] = fmaxf(mx[r], mx[r + w]);
-    const float tmax = halves_max(mx[0]);
+    for (int i = 0; i < 10; ++i) m1[i] = max3(v[3 * i], v[3 * i + 1], v[3 * i + 2]);
+    m1[10] = v[30];
+    m1[11] = v[31];
+    const float m2a = max3(m1[0], m1[1], m1[2]), m2b = max3(m1[3], m1[4], m1[5]);
+    const float m2c = max3(m1[6], m1[7], m1[8]), m2d = max3(m1[9], m1[10], m1[11]);
+    const float tmax = halves_max(max3(m2a, m2b, fmaxf(m2c, m2d)));
     const bool raise = tmax * p.scale_log2 > st.m_run * p.scale_log2 + kRescaleSlack;
     if (__any(raise)) {
         const float m_new = raise ? tmax : st.m_run;
@@ -596,8 +609,7 @@ __device__ __forceinline__ void softmax_phase(WaveState<D> &st, const AttnParams
             ps[e & 3] += x;
             st.pb[kk][e] = (__bf16)x;
         }
-    const float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
-    st.l_run += psum;
+    st.l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
 }
 
 // Barrier between the phases of the two wave groups; nothing is scheduled
@@ -648,6 +660,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
 
     int pos = start;
     int seg_no = 0;
+    int anc_b = -1;                 // sequence whose ancestor sets are in g_anc
     while (pos < end) {
         // ---- locate the unit holding tile `pos`
         int lo = 0, hi = p.B - 1;
@@ -656,7 +669,8 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             if (g_cum[mid] <= pos) lo = mid; else hi = mid - 1;
         }
         const int b = lo;
-        const int L = clamp_len(p.kv_len[b], p);
+        // scalar load: this path does not queue behind the tile loads
+        const int L = clamp_len(((const CONST_AS int32_t *)p.kv_len)[b], p);
         const int ntp = (L + KT - 1) / KT;
         const int per_g = p.row_blocks * ntp + p.tree_tiles_all_blocks;
         int off = pos - g_cum[b];
@@ -712,7 +726,12 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                 if (t_cov < ntp) tb = min(tb, t_cov);
             }
             const bool first = (ta == t0);
-            load_pages_and_parents<NT>(p, b, page_first, npages, ta < ntp, first && has_tree);
+            // page ids in LDS only for pages shorter than a load block; ancestor
+            // sets only when this piece reaches the tree tiles and the workgroup
+            // has not built them for this sequence already
+            const bool want_anc = first && has_tree && anc_b != b;
+            if ((SMALL && ta < ntp) || want_anc)
+                load_pages_and_parents<NT>(p, b, page_first, npages, SMALL && ta < ntp, want_anc);
 
             const int T = tb - ta;
             // Load batch i = K tile ta+i and V tile ta+i-1 (those that exist). It is
@@ -748,16 +767,24 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             };
             auto fetch = [&](int i) { ld.fetch_pages(p, b, ta + i, wave_u, pk); };
 
-            __builtin_amdgcn_s_waitcnt(0);  // Q, ids and earlier stores drained
+            // Q (issued above) and the first tiles are in flight together: the
+            // first tile wait below also covers Q, which was issued earlier.
             ld.set_unit(p, b, g, L, ntp);
-            fetch(0);
-            issue_batch(0);
-            fetch(1);
-            issue_batch(1);
-            fetch(2);
-            issue_batch(2);
-            fetch(3);
-            if (first && has_tree) build_ancestor_masks<NT>(p);   // overlaps the loads above
+            {
+                int ids[4][LPT];
+                #pragma unroll
+                for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, ta + i, wave_u, ids[i]);
+                #pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    #pragma unroll
+                    for (int k = 0; k < LPT; ++k) pk[k] = ids[i][k];
+                    if (i < 3) issue_batch(i);    // pk then holds the ids of batch 3
+                }
+            }
+            if (want_anc) {
+                build_ancestor_masks<NT>(p);   // overlaps the loads above
+                anc_b = b;
+            }
 
             // Slots of half a tile period, separated by workgroup barriers. Group 0
             // runs matrix j in slot 2j and softmax j in slot 2j+1; group 1 runs
