@@ -121,9 +121,13 @@ __device__ __forceinline__ int tree_tiles_of_block(int rb, const AttnParams &p) 
     return (jmax + KT - 1) / KT;
 }
 
+// Work of sequence b in "virtual" tiles: every unit counts setup_tiles in
+// front of its real tiles (the cost of starting a piece: its set-up and its
+// pipeline fill), so that equal shares of virtual tiles balance the work of
+// workgroups that start new units against those that do not.
 __device__ __forceinline__ int tiles_of_sequence(int b, const AttnParams &p) {
     const int L = clamp_len(p.kv_len[b], p);
-    return p.Hkv * (p.row_blocks * ((L + KT - 1) / KT) + p.tree_tiles_all_blocks);
+    return p.Hkv * (p.row_blocks * ((L + KT - 1) / KT + p.setup_tiles) + p.tree_tiles_all_blocks);
 }
 
 // Explicit LDS wait for reads issued through inline assembly; `tie` makes a
@@ -659,7 +663,6 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
     const unsigned v_lane = vb * Gm::kRowBytes + ((va ^ swz<Gm::kChunks>(vb)) << 4) + (lane & 1) * 8;
 
     int pos = start;
-    int seg_no = 0;
     int anc_b = -1;                 // sequence whose ancestor sets are in g_anc
     while (pos < end) {
         // ---- locate the unit holding tile `pos`
@@ -672,19 +675,26 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         // scalar load: this path does not queue behind the tile loads
         const int L = clamp_len(((const CONST_AS int32_t *)p.kv_len)[b], p);
         const int ntp = (L + KT - 1) / KT;
-        const int per_g = p.row_blocks * ntp + p.tree_tiles_all_blocks;
+        const int C = p.setup_tiles;
+        const int per_g = p.row_blocks * (ntp + C) + p.tree_tiles_all_blocks;
         int off = pos - g_cum[b];
         const int g = off / per_g;
         off -= g * per_g;
         int rb = 0;
-        int ulen = ntp + tree_tiles_of_block(0, p);
-        while (off >= ulen) {
-            off -= ulen;
+        int ulen = ntp + tree_tiles_of_block(0, p);     // real tiles of the unit
+        while (off >= C + ulen) {
+            off -= C + ulen;
             ++rb;
             ulen = ntp + tree_tiles_of_block(rb, p);
         }
-        const int t0 = off;
-        const int t_end = min(ulen, off + (end - pos));
+        // this share covers virtual tiles [off, v_end) of the unit; real tile
+        // r is virtual tile C + r
+        const int v_end = min(C + ulen, off + (end - pos));
+        const int unit_real_start = pos - off + C;    // share coordinate of real tile 0
+        pos += v_end - off;
+        const int t0 = max(off - C, 0);
+        const int t_end = v_end - C;
+        if (t_end <= t0) continue;                    // only set-up tiles of this unit
         const bool complete = (t0 == 0 && t_end == ulen);
 
         // ---- this wave's 32 query rows: Q fragments stay in registers
@@ -905,7 +915,8 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                         st.m_run * p.scale + __builtin_amdgcn_logf(l_tot) * kLn2;
             }
         } else {
-            const int slot = w * 2 + (seg_no == 0 ? 0 : 1);
+            // slot 0: the piece that continues a unit from before this share
+            const int slot = w * 2 + (unit_real_start <= start ? 0 : 1);
             const int rloc = wave_u * kRowsPerWave + col;
             float *po = p.ws_o + ((size_t)slot * p.rows_per_block + rloc) * D;
             #pragma unroll
@@ -922,8 +933,6 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                 pm[1] = l_tot;
             }
         }
-        pos += t_end - t0;
-        ++seg_no;
     }
 }
 
@@ -943,9 +952,10 @@ __global__ __launch_bounds__(256) void tree_attention_merge_kernel(AttnParams p)
     const int share = (total + p.num_wg - 1) / p.num_wg;
     const int L = clamp_len(p.kv_len[b], p);
     const int ntp = (L + KT - 1) / KT;
-    int ustart = p.ws_cum[b] + g * (p.row_blocks * ntp + p.tree_tiles_all_blocks);
-    for (int r = 0; r < rb; ++r) ustart += ntp + tree_tiles_of_block(r, p);
-    const int ulen = ntp + tree_tiles_of_block(rb, p);
+    const int C = p.setup_tiles;
+    int ustart = p.ws_cum[b] + g * (p.row_blocks * (ntp + C) + p.tree_tiles_all_blocks) + C;
+    for (int r = 0; r < rb; ++r) ustart += C + ntp + tree_tiles_of_block(r, p);
+    const int ulen = ntp + tree_tiles_of_block(rb, p);    // real tiles from ustart
     const int wf = ustart / share;
     const int wl = (ustart + ulen - 1) / share;
     if (wf == wl) return;

@@ -14,6 +14,7 @@ namespace {
 constexpr int kMaxDevices = 64;
 constexpr int kWgPerCu = 1;          // the attention kernel's LDS ring allows one workgroup per CU
 constexpr int kMinShareTiles = 8;    // smallest per-workgroup share worth a partial
+constexpr int kSetupTiles = 6;       // measured cost of starting a unit piece, in 64-key tiles
 constexpr int kArgmaxMinWorkgroups = 2048;
 constexpr int kArgmaxMinSegment = 4096;
 
@@ -158,16 +159,16 @@ int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
     const AttnWorkspace ws = attn_workspace(B, s, D, max_wg);
     if (workspace_bytes < ws.total) return TV_ERR_WORKSPACE;
 
-    // the tile count of the whole launch must fit in int32 for any kv_len
+    // the (virtual) tile count of the whole launch must fit in int32 for any kv_len
     const long max_len = (long)max_pages * P;
     const long worst = (long)B * Hkv *
-                       ((long)s.row_blocks * ((max_len + tv::kKeyTile - 1) / tv::kKeyTile) +
+                       ((long)s.row_blocks * ((max_len + tv::kKeyTile - 1) / tv::kKeyTile + kSetupTiles) +
                         s.tree_tiles_all);
     if (worst >= (1l << 30)) return TV_ERR_SHAPE;
 
     const long hint_len = max_kv_len < max_len ? max_kv_len : max_len;
     const long est = (long)B * Hkv *
-                     ((long)s.row_blocks * ((hint_len + tv::kKeyTile - 1) / tv::kKeyTile) +
+                     ((long)s.row_blocks * ((hint_len + tv::kKeyTile - 1) / tv::kKeyTile + kSetupTiles) +
                       s.tree_tiles_all);
     long num_wg = est / kMinShareTiles;
     if (num_wg < 1) num_wg = 1;
@@ -186,6 +187,7 @@ int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
     p.max_pages = max_pages; p.num_pages = num_pages;
     p.rows_per_block = s.rows_per_block; p.row_blocks = s.row_blocks;
     p.tree_tiles_all_blocks = s.tree_tiles_all;
+    p.setup_tiles = kSetupTiles;
     p.small_pages = P < 1024 / (2 * D) ? 1 : 0;
     p.num_wg = (int)num_wg;
     const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)D);

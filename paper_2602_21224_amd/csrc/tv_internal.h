@@ -34,6 +34,7 @@ struct AttnParams {
     int rows_per_block, row_blocks;
     int small_pages;             // pages shorter than one 1 KB load block of keys
     int tree_tiles_all_blocks;   // sum over row blocks of the tree tiles each needs
+    int setup_tiles;             // cost of starting a unit piece, in tiles (work balance)
     int num_wg;
     float scale_log2;            // softmax scale * log2(e)
     float scale;                 // softmax scale
