@@ -15,8 +15,9 @@
 //     All units' tiles are laid end to end and the workgroups take equal
 //     contiguous shares, so ragged prefixes stay balanced. A workgroup that
 //     covers a whole unit writes the output directly; a split unit leaves
-//     per-piece (max, sum, numerator) partials that a second kernel merges with
-//     the usual log-sum-exp rescaling.
+//     per-piece partials (max and sum in fp32, the piece's own normalised
+//     output in bf16) that a second kernel merges with the usual log-sum-exp
+//     rescaling.
 //   * K and V tiles stream from HBM straight into a 4-stage LDS ring with
 //     global_load_lds_dwordx4 (no register staging), three tiles ahead of the
 //     one being computed. Each 256-byte row is stored with its 16-byte chunks
@@ -645,8 +646,6 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
     const int w = xcd_contiguous_id(blockIdx.x, p.num_wg);
 
     build_cumulative<NT>(p);
-    if (w == 0)
-        for (int b = tid; b <= p.B; b += NT) p.ws_cum[b] = g_cum[b];
 
     const int total = g_cum[p.B];
     const int share = (total + p.num_wg - 1) / p.num_wg;
@@ -664,6 +663,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
 
     int pos = start;
     int anc_b = -1;                 // sequence whose ancestor sets are in g_anc
+    if (start >= end && tid == 0) p.ws_desc[w * 4] = -1;
     while (pos < end) {
         // ---- locate the unit holding tile `pos`
         int lo = 0, hi = p.B - 1;
@@ -691,6 +691,14 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         // r is virtual tile C + r
         const int v_end = min(C + ulen, off + (end - pos));
         const int unit_real_start = pos - off + C;    // share coordinate of real tile 0
+        if (pos == start && tid == 0) {
+            // the merge kernel's entry for this workgroup: the split unit whose
+            // last piece is this share's first, if any
+            const int wf = unit_real_start / share;
+            const bool mine = unit_real_start < start && (unit_real_start + ulen - 1) / share == w;
+            *reinterpret_cast<i32x4 *>(p.ws_desc + w * 4) =
+                mine ? i32x4{b, g, rb, wf * 2 + (unit_real_start <= wf * share ? 0 : 1)} : i32x4{-1, 0, 0, 0};
+        }
         pos += v_end - off;
         const int t0 = max(off - C, 0);
         const int t_end = v_end - C;
@@ -915,17 +923,22 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                         st.m_run * p.scale + __builtin_amdgcn_logf(l_tot) * kLn2;
             }
         } else {
-            // slot 0: the piece that continues a unit from before this share
+            // A piece of a split unit: its output normalised by its own sum, in
+            // bf16, plus the (max, sum) pair in fp32. Slot 0 holds the piece that
+            // continues a unit from before this share, slot 1 the one that starts
+            // inside it.
             const int slot = w * 2 + (unit_real_start <= start ? 0 : 1);
             const int rloc = wave_u * kRowsPerWave + col;
-            float *po = p.ws_o + ((size_t)slot * p.rows_per_block + rloc) * D;
+            uint16_t *po = p.ws_o + ((size_t)slot * p.rows_per_block + rloc) * D;
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
             #pragma unroll
             for (int dt = 0; dt < NDT; ++dt)
                 #pragma unroll
                 for (int q4 = 0; q4 < 4; ++q4) {
-                    f32x4 v = {st.o[dt][q4 * 4 + 0], st.o[dt][q4 * 4 + 1], st.o[dt][q4 * 4 + 2],
-                               st.o[dt][q4 * 4 + 3]};
-                    *reinterpret_cast<f32x4 *>(po + dt * 32 + q4 * 8 + half * 4) = v;
+                    bf16x4 v;
+                    #pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = (__bf16)(st.o[dt][q4 * 4 + i] * inv);
+                    *reinterpret_cast<bf16x4 *>(po + dt * 32 + q4 * 8 + half * 4) = v;
                 }
             if (half == 0) {
                 float *pm = p.ws_ml + ((size_t)slot * p.rows_per_block + rloc) * 2;
@@ -936,59 +949,56 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
     }
 }
 
-// Merge the partials of every unit that more than one workgroup worked on:
-// one thread per (row, 4 head-dim lanes) of the unit.
+// Merge the pieces of every split unit. Block (chunk, h) serves the workgroup
+// w that ran as block h of the main kernel, so it sits on the same XCD and
+// finds the newest partials in that XCD's L2. If w finished a unit that began
+// in an earlier share, the block merges a chunk of that unit's rows: one
+// thread per (row, 8 head-dim lanes), pieces combined in workgroup order with
+// an online log-sum-exp rescale (one pass, all loads of a piece independent).
 template <int D>
-__global__ __launch_bounds__(256) void tree_attention_merge_kernel(AttnParams p) {
-    constexpr int D4 = D / 4;
-    constexpr int kRowsPerWg = 256 / D4;
-    const int chunks = (p.rows_per_block + kRowsPerWg - 1) / kRowsPerWg;
-    const int unit = blockIdx.x / chunks;
-    const int rchunk = blockIdx.x % chunks;
-    const int rb = unit % p.row_blocks;
-    const int g = (unit / p.row_blocks) % p.Hkv;
-    const int b = unit / (p.row_blocks * p.Hkv);
-    const int total = p.ws_cum[p.B];
-    const int share = (total + p.num_wg - 1) / p.num_wg;
-    const int L = clamp_len(p.kv_len[b], p);
-    const int ntp = (L + KT - 1) / KT;
-    const int C = p.setup_tiles;
-    int ustart = p.ws_cum[b] + g * (p.row_blocks * (ntp + C) + p.tree_tiles_all_blocks) + C;
-    for (int r = 0; r < rb; ++r) ustart += C + ntp + tree_tiles_of_block(r, p);
-    const int ulen = ntp + tree_tiles_of_block(rb, p);    // real tiles from ustart
-    const int wf = ustart / share;
-    const int wl = (ustart + ulen - 1) / share;
-    if (wf == wl) return;
+__global__ __launch_bounds__(256) void tree_attention_merge_kernel(AttnParams p, int stride) {
+    constexpr int D8 = D / 8;
+    constexpr int kRowsPerWg = 256 / D8;
+    const int h = blockIdx.x % stride;
+    const int rchunk = blockIdx.x / stride;
+    if (h >= p.num_wg) return;
+    const int w = xcd_contiguous_id(h, p.num_wg);
+    const i32x4 d = ((const CONST_AS i32x4 *)p.ws_desc)[w];
+    const int b = d[0];
+    if (b < 0) return;
+    const int g = d[1], rb = d[2], s0 = d[3];
+    const int wf = s0 >> 1;
 
-    const int rl = rchunk * kRowsPerWg + threadIdx.x / D4;
-    const int d4 = threadIdx.x % D4;
+    const int rl = rchunk * kRowsPerWg + threadIdx.x / D8;
+    const int d8 = threadIdx.x % D8;
     const int row = rb * p.rows_per_block + rl;
     if (rl >= p.rows_per_block || row >= p.rows) return;
 
-    float M = kNegInf;
-    for (int w = wf; w <= wl; ++w) {
-        const int slot = w * 2 + (ustart <= w * share ? 0 : 1);
-        M = fmaxf(M, p.ws_ml[((size_t)slot * p.rows_per_block + rl) * 2]);
-    }
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    float den = 0.f;
-    for (int w = wf; w <= wl; ++w) {
-        const int slot = w * 2 + (ustart <= w * share ? 0 : 1);
-        const float *pm = p.ws_ml + ((size_t)slot * p.rows_per_block + rl) * 2;
-        const float wt = (pm[0] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(pm[0] - M);
-        den += wt * pm[1];
-        const f32x4 v = *reinterpret_cast<const f32x4 *>(
-            p.ws_o + ((size_t)slot * p.rows_per_block + rl) * D + d4 * 4);
-        acc += wt * v;
+    float M = kNegInf, den = 0.f;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    #pragma unroll 4
+    for (int u = wf; u <= w; ++u) {
+        // the first piece may sit in slot 1 of its workgroup; later ones start a share
+        const int slot = u == wf ? s0 : u * 2;
+        const size_t r = (size_t)slot * p.rows_per_block + rl;
+        const f32x2 ml = *reinterpret_cast<const f32x2 *>(p.ws_ml + r * 2);
+        const bf16x8 v = *reinterpret_cast<const bf16x8 *>(p.ws_o + r * D + d8 * 8);
+        const float Mn = fmaxf(M, ml[0]);
+        const float sc = (M == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
+        const float wt = (ml[0] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ml[0] - Mn) * ml[1];
+        den = den * sc + wt;
+        #pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = acc[i] * sc + wt * (float)v[i];
+        M = Mn;
     }
     const int node = row / p.G;
     const int hq = g * p.G + row % p.G;
     const float inv = den > 0.f ? 1.f / den : 0.f;
-    bf16x4 v;
+    bf16x8 o;
     #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = (__bf16)(acc[i] * inv);
-    *reinterpret_cast<bf16x4 *>(p.out + (((size_t)b * p.N + node) * p.Hq + hq) * D + d4 * 4) = v;
-    if (p.lse && d4 == 0)
+    for (int i = 0; i < 8; ++i) o[i] = (__bf16)(acc[i] * inv);
+    *reinterpret_cast<bf16x8 *>(p.out + (((size_t)b * p.N + node) * p.Hq + hq) * D + d8 * 8) = o;
+    if (p.lse && d8 == 0)
         p.lse[((size_t)b * p.N + node) * p.Hq + hq] = (M + __builtin_amdgcn_logf(den)) * kLn2;
 }
 
@@ -1001,10 +1011,11 @@ hipError_t launch_dn(const AttnParams &p, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (p.num_wg > 1) {
-        constexpr int kRowsPerWg = 256 / (D / 4);
+        constexpr int kRowsPerWg = 256 / (D / 8);
         const int chunks = (p.rows_per_block + kRowsPerWg - 1) / kRowsPerWg;
-        hipLaunchKernelGGL((tree_attention_merge_kernel<D>),
-                           dim3(p.B * p.Hkv * p.row_blocks * chunks), dim3(256), 0, s, p);
+        const int stride = (p.num_wg + kNumXcd - 1) / kNumXcd * kNumXcd;
+        hipLaunchKernelGGL((tree_attention_merge_kernel<D>), dim3(stride * chunks), dim3(256), 0, s, p,
+                           stride);
         e = hipGetLastError();
     }
     return e;

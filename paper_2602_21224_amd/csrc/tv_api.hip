@@ -73,15 +73,15 @@ AttnShape attn_shape(int N, int Hq, int Hkv) {
 }
 
 struct AttnWorkspace {
-    size_t o_bytes, ml_bytes, cum_bytes, total;
+    size_t o_bytes, ml_bytes, desc_bytes, total;
 };
 
-AttnWorkspace attn_workspace(int B, const AttnShape &s, int D, int max_wg) {
+AttnWorkspace attn_workspace(const AttnShape &s, int D, int max_wg) {
     AttnWorkspace w;
-    w.o_bytes = round_up((size_t)max_wg * 2 * s.rows_per_block * D * sizeof(float), 256);
+    w.o_bytes = round_up((size_t)max_wg * 2 * s.rows_per_block * D * sizeof(uint16_t), 256);
     w.ml_bytes = round_up((size_t)max_wg * 2 * s.rows_per_block * 2 * sizeof(float), 256);
-    w.cum_bytes = round_up((size_t)(B + 1) * sizeof(int32_t), 256);
-    w.total = w.o_bytes + w.ml_bytes + w.cum_bytes;
+    w.desc_bytes = round_up((size_t)max_wg * 4 * sizeof(int32_t), 256);
+    w.total = w.o_bytes + w.ml_bytes + w.desc_bytes;
     return w;
 }
 
@@ -133,7 +133,7 @@ const char *tv_status_string(int status) {
 size_t tv_attention_workspace_size(int B, int N, int Hq, int Hkv, int D) {
     if (!attn_shape_ok(B, N, Hq, Hkv, D)) return 0;
     const AttnShape s = attn_shape(N, Hq, Hkv);
-    return attn_workspace(B, s, D, cu_count() * kWgPerCu).total;
+    return attn_workspace(s, D, cu_count() * kWgPerCu).total;
 }
 
 int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
@@ -156,7 +156,7 @@ int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
 
     const AttnShape s = attn_shape(N, Hq, Hkv);
     const int max_wg = cu_count() * kWgPerCu;
-    const AttnWorkspace ws = attn_workspace(B, s, D, max_wg);
+    const AttnWorkspace ws = attn_workspace(s, D, max_wg);
     if (workspace_bytes < ws.total) return TV_ERR_WORKSPACE;
 
     // the (virtual) tile count of the whole launch must fit in int32 for any kv_len
@@ -179,9 +179,9 @@ int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
     p.page_table = page_table; p.kv_len = kv_len; p.parent = parent;
     p.out = out; p.lse = lse;
     char *base = static_cast<char *>(workspace);
-    p.ws_o = reinterpret_cast<float *>(base);
+    p.ws_o = reinterpret_cast<uint16_t *>(base);
     p.ws_ml = reinterpret_cast<float *>(base + ws.o_bytes);
-    p.ws_cum = reinterpret_cast<int32_t *>(base + ws.o_bytes + ws.ml_bytes);
+    p.ws_desc = reinterpret_cast<int32_t *>(base + ws.o_bytes + ws.ml_bytes);
     p.B = B; p.N = N; p.Hq = Hq; p.Hkv = Hkv; p.G = s.G; p.rows = s.rows;
     p.P = P; p.p_shift = __builtin_ctz((unsigned)P);
     p.max_pages = max_pages; p.num_pages = num_pages;

@@ -10,6 +10,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
@@ -27,9 +29,9 @@ struct AttnParams {
     const int32_t *page_table, *kv_len, *parent;
     uint16_t *out;
     float *lse;
-    float *ws_o;       // [num_wg * 2][rows_per_block][D] partial numerators
+    uint16_t *ws_o;    // [num_wg * 2][rows_per_block][D] bf16 partial outputs (normalised)
     float *ws_ml;      // [num_wg * 2][rows_per_block][2] partial (max, sum)
-    int32_t *ws_cum;   // [B + 1] cumulative tile counts (written by workgroup 0)
+    int32_t *ws_desc;  // [num_wg][4] per workgroup: the split unit it finishes (b, g, rb, first slot), b < 0 if none
     int B, N, Hq, Hkv, G, rows, P, p_shift, max_pages, num_pages;
     int rows_per_block, row_blocks;
     int small_pages;             // pages shorter than one 1 KB load block of keys

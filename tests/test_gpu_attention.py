@@ -167,3 +167,32 @@ def test_understated_max_kv_len_hint_is_still_exact(oracle_mod):
     want, wlse = oracle_mod.tree_attention(w.q, w.k_tree, w.v_tree, w.k_cache, w.v_cache,
                                            w.page_table, w.kv_len, w.parent)
     U.assert_attention_close(U.bf16_to_f64(out), want, lse.cpu().numpy(), wlse, "hint0")
+
+
+def test_shared_workspace_alternating_inputs(oracle_mod):
+    """One workspace reused by calls on different inputs of one shape (units
+    split over several workgroups, so pieces meet in the workspace): every call
+    matches the oracle on its own inputs, and repeats are bit-identical."""
+    T = U.require_gpu()
+    ws_ = [wl(51 + k, B=4, N=64, Hq=32, Hkv=8, D=128, L=(500, 2000), tree="capped") for k in range(2)]
+    w0 = ws_[0]
+    need = T.attention_workspace_size(w0.B, w0.N, w0.Hq, w0.Hkv, w0.D)
+    work = torch.empty(need, dtype=torch.uint8, device="cuda")
+    work.fill_(0xFF)                       # contents on entry must not matter
+    dev_in = [U.upload(w) for w in ws_]
+    want = [oracle_mod.tree_attention(w.q, w.k_tree, w.v_tree, w.k_cache, w.v_cache,
+                                      w.page_table, w.kv_len, w.parent) for w in ws_]
+    first = [None, None]
+    for it in range(6):
+        k = it % 2
+        d, w = dev_in[k], ws_[k]
+        out, lse = T.tree_verify_attention(d["q"], d["k_tree"], d["v_tree"], d["k_cache"],
+                                           d["v_cache"], d["page_table"], d["kv_len"],
+                                           d["parent"], max_kv_len=w.max_kv_len, workspace=work)
+        torch.cuda.synchronize()
+        got, glse = U.bf16_to_f64(out), lse.cpu().numpy().astype(np.float64)
+        if first[k] is None:
+            U.assert_attention_close(got, want[k][0], glse, want[k][1], f"alt{it}")
+            first[k] = (got, glse)
+        else:
+            assert np.array_equal(got, first[k][0]) and np.array_equal(glse, first[k][1]), f"alt{it}"
