@@ -830,6 +830,10 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                     else wait_vmcnt<0>();
                 }
                 phase_barrier();
+                // The matrix phase runs at raised wave priority: when both waves of
+                // a SIMD could issue, its MFMAs and LDS reads go first and the other
+                // group's softmax fills the gaps.
+                __builtin_amdgcn_s_setprio(1);
                 const int i = j + 3;
                 have_k = have_v = false;
                 if (i <= T) {
@@ -875,6 +879,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                     if (j + 4 <= T) wait_vmcnt<4 * LPT < 63 ? 4 * LPT : 63>();
                     else wait_vmcnt<0>();
                 }
+                __builtin_amdgcn_s_setprio(0);
                 phase_barrier();
                 softmax_phase<D>(st, p, ta + j, ntp, L, node, half);
                 fetch(j + 4);          // ids for the batch issued at the next matrix phase
