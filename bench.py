@@ -76,6 +76,73 @@ def load_traffic(kernel: str, workload: str):
     return t.get("hbm_bytes_per_launch")
 
 
+CALL_KERNELS = {
+    "tree_verify_attention": ("tree_attention_kernel", "tree_attention_merge_kernel"),
+    "tree_argmax_accept": ("argmax_segments_kernel", "accept_kernel"),
+    "kv_compact_accepted": ("kv_compact_kernel",),
+}
+
+
+def _counter_means(run_dir: str, counter: str):
+    """Mean value per dispatch of one rocprofv3 counter, by kernel base name."""
+    import csv
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    vals = {}
+    for fn in files:
+        with open(fn) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                name = r["Kernel_Name"].replace("(anonymous namespace)", "")
+                base = name.split("(")[0].split("<")[0].split("::")[-1].split()[-1]
+                vals.setdefault(base, []).append(float(r["Counter_Value"]))
+    return vals
+
+
+def write_traffic(workload: str, fetch_dir: str, write_dir: str, copy_fetch_dir: str,
+                  copy_write_dir: str):
+    """Turn rocprofv3 FETCH_SIZE / WRITE_SIZE runs (KiB per dispatch) of this
+    benchmark and of --copy-calibration into HBM bytes per call, scaled by what
+    the same counters read for a device copy of known size, and store them under
+    profiles/ with the digest of the kernel sources they were taken on."""
+    cf = _counter_means(copy_fetch_dir, "FETCH_SIZE")["__amd_rocclr_copyBuffer"]
+    cw = _counter_means(copy_write_dir, "WRITE_SIZE")["__amd_rocclr_copyBuffer"]
+    copy_kib = float(1 << 30) / 1024.0
+    fetch_scale = copy_kib / max(cf)
+    write_scale = copy_kib / max(cw)
+    fv = _counter_means(fetch_dir, "FETCH_SIZE")
+    wv = _counter_means(write_dir, "WRITE_SIZE")
+    for call, kernels in CALL_KERNELS.items():
+        per = {}
+        total = 0.0
+        for k in kernels:
+            if k not in fv or k not in wv:
+                continue
+            fb = np.mean(fv[k]) * 1024.0 * fetch_scale
+            wb = np.mean(wv[k]) * 1024.0 * write_scale
+            per[k] = {"fetch_bytes": int(round(fb)), "write_bytes": int(round(wb)),
+                      "dispatches": len(fv[k])}
+            total += fb + wb
+        if not per:
+            continue
+        out = {"call": call, "workload": workload, "hbm_bytes_per_launch": int(round(total)),
+               "kernels": per, "fetch_scale": round(fetch_scale, 4),
+               "write_scale": round(write_scale, 4),
+               "calibration": f"1 GiB device copy: FETCH_SIZE {max(cf):.1f} KiB, "
+                              f"WRITE_SIZE {max(cw):.1f} KiB per launch",
+               "source_digest": source_digest()}
+        path = os.path.join(ROOT, "profiles", f"traffic_{call}_{workload}.json")
+        with open(path, "w") as fh:
+            json.dump(out, fh, indent=1)
+            fh.write("\n")
+        print(f"{call}: {total / 1e6:.2f} MB per call -> {os.path.relpath(path, ROOT)}")
+        for k, v in per.items():
+            print(f"   {k:30s} read {v['fetch_bytes'] / 1e6:9.2f} MB  written "
+                  f"{v['write_bytes'] / 1e6:8.2f} MB  ({v['dispatches']} dispatches)")
+
+
 def cpu_baseline(w, sample_b: int, min_seconds: float = 10.0):
     """The fp64 CPU oracle on the first `sample_b` sequences of the same workload."""
     import oracle
@@ -110,7 +177,15 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB a few times (calibrates "
                          "the HBM byte counters against a known size) and exit")
+    ap.add_argument("--write-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
+                                                      "COPY_WRITE_DIR"),
+                    help="convert rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE output directories "
+                         "(this benchmark, then --copy-calibration 1024) into "
+                         "profiles/traffic_*.json and exit; needs no GPU")
     args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(args.workload, *args.write_traffic)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the verification "
               "step shards by sequence with no exchange, so N GPUs run N independent copies.",
