@@ -106,6 +106,7 @@ __shared__ int g_par[kMaxNodes];
 __shared__ int g_jump[2][kMaxNodes];
 __shared__ int g_pages[kPageCache];
 __shared__ int g_cum[kMaxBatchAttn + 1];
+__shared__ int g_len[kMaxBatchAttn];     // clamped prefix length per sequence
 
 __device__ __forceinline__ unsigned lds_addr(const void *p) {
     return (unsigned)(size_t)(const LDS_AS void *)p;
@@ -126,8 +127,7 @@ __device__ __forceinline__ int tree_tiles_of_block(int rb, const AttnParams &p) 
 // front of its real tiles (the cost of starting a piece: its set-up and its
 // pipeline fill), so that equal shares of virtual tiles balance the work of
 // workgroups that start new units against those that do not.
-__device__ __forceinline__ int tiles_of_sequence(int b, const AttnParams &p) {
-    const int L = clamp_len(p.kv_len[b], p);
+__device__ __forceinline__ int tiles_of_len(int L, const AttnParams &p) {
     return p.Hkv * (p.row_blocks * ((L + KT - 1) / KT + p.setup_tiles) + p.tree_tiles_all_blocks);
 }
 
@@ -166,30 +166,32 @@ __device__ __forceinline__ void wait_tile_loads(int newer_tiles, int loads_per_t
     else wait_vmcnt<0>();
 }
 
-// Exclusive prefix sum of per-sequence tile counts into g_cum[0..B].
+// Exclusive prefix sum of per-sequence tile counts into g_cum[0..B] and the
+// clamped prefix lengths into g_len[0..B): wave 0 reads kv_len once per lane
+// and scans with cross-lane shifts, one barrier for the whole workgroup.
 template <int NT>
 __device__ void build_cumulative(const AttnParams &p) {
-    const int tid = threadIdx.x;
-    const int per = (p.B + NT - 1) / NT;
-    const int b0 = tid * per;
-    const int b1 = min(b0 + per, p.B);
-    int local = 0;
-    for (int b = b0; b < b1; ++b) local += tiles_of_sequence(b, p);
-    int *scan = &g_jump[0][0];            // 2 * kMaxNodes >= NT ints of scratch
-    scan[tid] = local;
-    __syncthreads();
-    for (int off = 1; off < NT; off <<= 1) {
-        const int v = tid >= off ? scan[tid - off] : 0;
-        __syncthreads();
-        scan[tid] += v;
-        __syncthreads();
+    if (threadIdx.x < kWave) {
+        const int lane = threadIdx.x;
+        int carry = 0;
+        for (int b0 = 0; b0 < p.B; b0 += kWave) {
+            const int b = b0 + lane;
+            const int L = b < p.B ? clamp_len(p.kv_len[b], p) : 0;
+            const int t = b < p.B ? tiles_of_len(L, p) : 0;
+            int x = t;                                   // inclusive scan over the wave
+            #pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const int y = __shfl_up(x, off);
+                if (lane >= off) x += y;
+            }
+            if (b < p.B) {
+                g_cum[b] = carry + x - t;
+                g_len[b] = L;
+            }
+            carry += __shfl(x, kWave - 1);
+        }
+        if (lane == 0) g_cum[p.B] = carry;
     }
-    int run = scan[tid] - local;
-    for (int b = b0; b < b1; ++b) {
-        g_cum[b] = run;
-        run += tiles_of_sequence(b, p);
-    }
-    if (tid == NT - 1) g_cum[p.B] = scan[NT - 1];
     __syncthreads();
 }
 
@@ -672,8 +674,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             if (g_cum[mid] <= pos) lo = mid; else hi = mid - 1;
         }
         const int b = lo;
-        // scalar load: this path does not queue behind the tile loads
-        const int L = clamp_len(((const CONST_AS int32_t *)p.kv_len)[b], p);
+        const int L = g_len[b];
         const int ntp = (L + KT - 1) / KT;
         const int C = p.setup_tiles;
         const int per_g = p.row_blocks * (ntp + C) + p.tree_tiles_all_blocks;
