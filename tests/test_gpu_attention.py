@@ -196,3 +196,14 @@ def test_shared_workspace_alternating_inputs(oracle_mod):
             first[k] = (got, glse)
         else:
             assert np.array_equal(got, first[k][0]) and np.array_equal(glse, first[k][1]), f"alt{it}"
+
+
+@pytest.mark.parametrize("B,N,Hq,Hkv,D,L", [
+    (130, 4, 8, 2, 64, (0, 200)),       # sequence count spans several 64-wide scan chunks
+    (1024, 2, 4, 4, 64, (0, 70)),       # the largest supported batch
+    (1, 256, 64, 8, 128, 300),          # (Hq / Hkv) * N = 2048 rows: eight row blocks
+])
+def test_batch_and_row_extremes(oracle_mod, B, N, Hq, Hkv, D, L):
+    T = U.require_gpu()
+    w = wl(61 + B, B=B, N=N, Hq=Hq, Hkv=Hkv, D=D, L=L, tree="capped")
+    full_compare(oracle_mod, T, w, f"extreme_B{B}_N{N}_G{Hq // Hkv}")
