@@ -650,9 +650,15 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
     build_cumulative<NT>(p);
 
     const int total = g_cum[p.B];
-    const int share = (total + p.num_wg - 1) / p.num_wg;
-    const int start = min(w * share, total);
-    const int end = min(start + share, total);
+    // Workgroup u < nw takes virtual tiles [share_start(u), share_start(u + 1)):
+    // shares differ by at most one tile and none is empty (nw <= total), so the
+    // pieces of a split unit sit in consecutive workgroups. Workgroups past nw
+    // (only when the length hint overstated the work) have nothing to do.
+    const int nw = min(p.num_wg, total);
+    auto share_start = [&](int u) { return (int)(((long long)min(u, nw) * total) / max(nw, 1)); };
+    auto share_of = [&](int t) { return (int)(((long long)(t + 1) * nw - 1) / total); };
+    const int start = share_start(w);
+    const int end = share_start(w + 1);
     const unsigned ring_base = lds_addr(g_ring);
     Issue ld;
     ld.init(wave_u, lane, p);
@@ -695,10 +701,11 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         if (pos == start && tid == 0) {
             // the merge kernel's entry for this workgroup: the split unit whose
             // last piece is this share's first, if any
-            const int wf = unit_real_start / share;
-            const bool mine = unit_real_start < start && (unit_real_start + ulen - 1) / share == w;
+            const int wf = share_of(unit_real_start);
+            const bool mine = unit_real_start < start && share_of(unit_real_start + ulen - 1) == w;
             *reinterpret_cast<i32x4 *>(p.ws_desc + w * 4) =
-                mine ? i32x4{b, g, rb, wf * 2 + (unit_real_start <= wf * share ? 0 : 1)} : i32x4{-1, 0, 0, 0};
+                mine ? i32x4{b, g, rb, wf * 2 + (unit_real_start <= share_start(wf) ? 0 : 1)}
+                     : i32x4{-1, 0, 0, 0};
         }
         pos += v_end - off;
         const int t0 = max(off - C, 0);
