@@ -41,14 +41,14 @@ def _load():
         lib = ctypes.CDLL(_LIB)
         p = ctypes.c_void_p
         i = ctypes.c_int
-        lib.oracle_tree_attention.argtypes = [p] * 8 + [i] * 8 + [ctypes.c_double, p, p]
+        lib.oracle_tree_attention.argtypes = [p] * 9 + [i] * 8 + [ctypes.c_double, p, p]
         lib.oracle_tree_attention.restype = i
-        lib.oracle_tree_attention_rows.argtypes = [p] * 8 + [i] * 8 + [ctypes.c_double, p, i,
+        lib.oracle_tree_attention_rows.argtypes = [p] * 9 + [i] * 8 + [ctypes.c_double, p, i,
                                                                         p, p]
         lib.oracle_tree_attention_rows.restype = i
         lib.oracle_argmax.argtypes = [p, ctypes.c_long, ctypes.c_long, p]
         lib.oracle_argmax.restype = None
-        lib.oracle_accept.argtypes = [p, p, p, i, i, p, p, p]
+        lib.oracle_accept.argtypes = [p, p, p, p, i, i, p, p, p]
         lib.oracle_accept.restype = i
         lib.oracle_kv_compact.argtypes = [p] * 8 + [i] * 7
         lib.oracle_kv_compact.restype = i
@@ -67,16 +67,32 @@ def _c(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
 
 
+def _opt(a, n):
+    """Optional per-sequence int32 array of length n, or None."""
+    if a is None:
+        return None
+    a = _c(a, np.int32).reshape(-1)
+    if a.shape[0] != n:
+        raise ValueError("num_nodes must hold one count per sequence")
+    return a
+
+
+def _optr(a):
+    return None if a is None else _ptr(a)
+
+
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
 
 
 def tree_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent,
-                   scale: float = 0.0):
+                   scale: float = 0.0, num_nodes=None):
     """Tree-masked attention (§2.1 tree-shaped verification mask; §8 SpecInfer
     masking; §1 attention over all cached keys). Inputs are bf16 bit arrays in
     the layouts of `paper_2602_21224_amd.workloads`. Returns (out, lse) as fp64
-    arrays [B, N, Hq, D] and [B, N, Hq]."""
+    arrays [B, N, Hq, D] and [B, N, Hq]. `num_nodes` [B] (optional) gives each
+    sequence's node count, e.g. a verification-fusion forest (§6.2) padded to
+    N; rows of the padding nodes are zeros with lse -inf."""
     q = _c(q, np.uint16)
     k_tree = _c(k_tree, np.uint16)
     v_tree = _c(v_tree, np.uint16)
@@ -89,11 +105,12 @@ def tree_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, pare
     Hkv = k_tree.shape[2]
     num_pages, P = k_cache.shape[0], k_cache.shape[1]
     max_pages = page_table.shape[1]
+    nn = _opt(num_nodes, B)
     out = np.zeros((B, N, Hq, D), dtype=np.float64)
     lse = np.zeros((B, N, Hq), dtype=np.float64)
     rc = _load().oracle_tree_attention(
         _ptr(q), _ptr(k_tree), _ptr(v_tree), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
-        _ptr(kv_len), _ptr(parent), B, N, Hq, Hkv, D, P, max_pages, num_pages,
+        _ptr(kv_len), _ptr(parent), _optr(nn), B, N, Hq, Hkv, D, P, max_pages, num_pages,
         float(scale), _ptr(out), _ptr(lse))
     if rc != 0:
         raise ValueError("oracle_tree_attention rejected its arguments")
@@ -101,7 +118,7 @@ def tree_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, pare
 
 
 def tree_attention_rows(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, items,
-                        scale: float = 0.0):
+                        scale: float = 0.0, num_nodes=None):
     """The same attention for selected (b, i, h) rows only; items is an int
     array [n, 3]. Returns (out [n, D], lse [n]) in fp64."""
     q = _c(q, np.uint16)
@@ -116,11 +133,12 @@ def tree_attention_rows(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len,
     B, N, Hq, D = q.shape
     Hkv = k_tree.shape[2]
     num_pages, P = k_cache.shape[0], k_cache.shape[1]
+    nn = _opt(num_nodes, B)
     out = np.zeros((len(items), D), dtype=np.float64)
     lse = np.zeros(len(items), dtype=np.float64)
     rc = _load().oracle_tree_attention_rows(
         _ptr(q), _ptr(k_tree), _ptr(v_tree), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
-        _ptr(kv_len), _ptr(parent), B, N, Hq, Hkv, D, P, page_table.shape[1], num_pages,
+        _ptr(kv_len), _ptr(parent), _optr(nn), B, N, Hq, Hkv, D, P, page_table.shape[1], num_pages,
         float(scale), _ptr(items), len(items), _ptr(out), _ptr(lse))
     if rc != 0:
         raise ValueError("oracle_tree_attention_rows rejected its arguments")
@@ -138,17 +156,20 @@ def argmax(logits):
     return out
 
 
-def accept(draft, parent, amax):
+def accept(draft, parent, amax, num_nodes=None):
     """Greedy longest accepted path and bonus token (§5.3; Alg. 2's
-    ground-truth token). Returns (accept_len [B], accept_idx [B, N], bonus [B])."""
+    ground-truth token). Returns (accept_len [B], accept_idx [B, N], bonus [B]).
+    With `num_nodes` only each sequence's first num_nodes[b] nodes take part;
+    a sequence with none accepts nothing (length 0, bonus -1)."""
     draft = _c(draft, np.int32)
     parent = _c(parent, np.int32)
     amax = _c(amax, np.int32)
     B, N = parent.shape
+    nn = _opt(num_nodes, B)
     alen = np.zeros(B, dtype=np.int32)
     aidx = np.zeros((B, N), dtype=np.int32)
     bonus = np.zeros(B, dtype=np.int32)
-    rc = _load().oracle_accept(_ptr(draft), _ptr(parent), _ptr(amax), B, N,
+    rc = _load().oracle_accept(_ptr(draft), _ptr(parent), _ptr(amax), _optr(nn), B, N,
                                _ptr(alen), _ptr(aidx), _ptr(bonus))
     if rc != 0:
         raise ValueError("oracle_accept: parent[i] must lie in [-1, i-1]")

@@ -66,14 +66,24 @@ int oracle_num_threads(void)
 #endif
 }
 
-/* Argument checks shared by the attention entry points. */
+/* Node count of sequence b: num_nodes[b] when given, else N. */
+static int nodes_of(const int32_t *num_nodes, int N, int b)
+{
+    return num_nodes ? num_nodes[b] : N;
+}
+
+/* Argument checks shared by the attention entry points. Nodes at or past a
+ * sequence's node count are padding: their parents are not looked at. */
 static int attention_args_ok(const int32_t *page_table, const int32_t *kv_len,
-                             const int32_t *parent, int B, int N, int Hq, int Hkv, int D, int P,
-                             int max_pages, int num_pages)
+                             const int32_t *parent, const int32_t *num_nodes, int B, int N,
+                             int Hq, int Hkv, int D, int P, int max_pages, int num_pages)
 {
     if (B < 0 || N < 1 || Hq < 1 || Hkv < 1 || D < 1 || P < 1 || Hq % Hkv != 0)
         return 0;
     for (int b = 0; b < B; ++b) {
+        const int nb = nodes_of(num_nodes, N, b);
+        if (nb < 0 || nb > N)
+            return 0;
         int L = kv_len[b];
         if (L < 0 || (L + P - 1) / P > max_pages)
             return 0;
@@ -82,13 +92,23 @@ static int attention_args_ok(const int32_t *page_table, const int32_t *kv_len,
             if (pg < 0 || pg >= num_pages)
                 return 0;
         }
-        for (int i = 0; i < N; ++i) {
+        for (int i = 0; i < nb; ++i) {
             int p = parent[(long)b * N + i];
             if (p < -1 || p >= i)
                 return 0;
         }
     }
     return 1;
+}
+
+/* One output row of a padding node: zeros, and the log-sum-exp of an empty
+ * key set. */
+static void padding_row(int D, double *o, double *lse_out)
+{
+    for (int d = 0; d < D; ++d)
+        o[d] = 0.0;
+    if (lse_out)
+        *lse_out = -INFINITY;
 }
 
 /* One output row: node i of sequence b, query head h. Writes D values to o
@@ -159,15 +179,19 @@ static void attend_one(const uint16_t *q, const uint16_t *k_tree, const uint16_t
 /* Tree-masked attention of every node's query heads over the paged prefix
  * plus the node's own root path. Outputs are fp64:
  *   out [B, N, Hq, D], lse [B, N, Hq] (natural log of sum_j exp(s_j)).
- * Returns 0, or -1 on a malformed argument (nothing written). */
+ * num_nodes (may be NULL: every sequence has N nodes) gives each sequence's
+ * node count; rows of the nodes past it are padding (zeros, lse -inf) and no
+ * padding input is read. Returns 0, or -1 on a malformed argument (nothing
+ * written). */
 int oracle_tree_attention(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
                           const uint16_t *k_cache, const uint16_t *v_cache,
                           const int32_t *page_table, const int32_t *kv_len,
-                          const int32_t *parent, int B, int N, int Hq, int Hkv, int D,
-                          int P, int max_pages, int num_pages, double scale,
+                          const int32_t *parent, const int32_t *num_nodes, int B, int N, int Hq,
+                          int Hkv, int D, int P, int max_pages, int num_pages, double scale,
                           double *out, double *lse)
 {
-    if (!attention_args_ok(page_table, kv_len, parent, B, N, Hq, Hkv, D, P, max_pages, num_pages))
+    if (!attention_args_ok(page_table, kv_len, parent, num_nodes, B, N, Hq, Hkv, D, P, max_pages,
+                           num_pages))
         return -1;
     if (!(scale > 0.0))
         scale = 1.0 / sqrt((double)D);
@@ -177,9 +201,12 @@ int oracle_tree_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
         for (int i = 0; i < N; ++i)
             for (int h = 0; h < Hq; ++h) {
                 long row = ((long)b * N + i) * Hq + h;
-                attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, N,
-                           Hq, Hkv, D, P, max_pages, scale, b, i, h, out + row * D,
-                           lse ? lse + row : NULL);
+                if (i >= nodes_of(num_nodes, N, b))
+                    padding_row(D, out + row * D, lse ? lse + row : NULL);
+                else
+                    attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent,
+                               N, Hq, Hkv, D, P, max_pages, scale, b, i, h, out + row * D,
+                               lse ? lse + row : NULL);
             }
     return 0;
 }
@@ -190,11 +217,13 @@ int oracle_tree_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
 int oracle_tree_attention_rows(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
                                const uint16_t *k_cache, const uint16_t *v_cache,
                                const int32_t *page_table, const int32_t *kv_len,
-                               const int32_t *parent, int B, int N, int Hq, int Hkv, int D, int P,
-                               int max_pages, int num_pages, double scale, const int32_t *items,
-                               int n_items, double *out_rows, double *lse_rows)
+                               const int32_t *parent, const int32_t *num_nodes, int B, int N,
+                               int Hq, int Hkv, int D, int P, int max_pages, int num_pages,
+                               double scale, const int32_t *items, int n_items, double *out_rows,
+                               double *lse_rows)
 {
-    if (!attention_args_ok(page_table, kv_len, parent, B, N, Hq, Hkv, D, P, max_pages, num_pages))
+    if (!attention_args_ok(page_table, kv_len, parent, num_nodes, B, N, Hq, Hkv, D, P, max_pages,
+                           num_pages))
         return -1;
     for (int k = 0; k < n_items; ++k) {
         const int32_t *it = items + 3L * k;
@@ -207,9 +236,12 @@ int oracle_tree_attention_rows(const uint16_t *q, const uint16_t *k_tree, const 
 #pragma omp parallel for schedule(dynamic, 1)
     for (int k = 0; k < n_items; ++k) {
         const int32_t *it = items + 3L * k;
-        attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, N, Hq, Hkv,
-                   D, P, max_pages, scale, it[0], it[1], it[2], out_rows + (long)k * D,
-                   lse_rows ? lse_rows + k : NULL);
+        if (it[1] >= nodes_of(num_nodes, N, it[0]))
+            padding_row(D, out_rows + (long)k * D, lse_rows ? lse_rows + k : NULL);
+        else
+            attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, N, Hq,
+                       Hkv, D, P, max_pages, scale, it[0], it[1], it[2], out_rows + (long)k * D,
+                       lse_rows ? lse_rows + k : NULL);
     }
     return 0;
 }
@@ -241,19 +273,27 @@ void oracle_argmax(const float *logits, long rows, long V, int32_t *out)
  *                 draft(i) == argmax(parent(i));
  *   the path ends at the accepted node of greatest depth (lowest index on a
  *   tie) and runs root first; bonus = argmax at its last node.
+ * num_nodes (may be NULL: N nodes each) limits each sequence to its first
+ * nodes; a sequence with none accepts nothing (length 0, bonus -1).
  * Returns 0, or -1 on a malformed tree. */
-int oracle_accept(const int32_t *draft, const int32_t *parent, const int32_t *amax, int B, int N,
-                  int32_t *accept_len, int32_t *accept_idx, int32_t *bonus)
+int oracle_accept(const int32_t *draft, const int32_t *parent, const int32_t *amax,
+                  const int32_t *num_nodes, int B, int N, int32_t *accept_len,
+                  int32_t *accept_idx, int32_t *bonus)
 {
     int status = 0;
     for (int b = 0; b < B; ++b) {
         const int32_t *par = parent + (long)b * N;
         const int32_t *tok = draft + (long)b * N;
         const int32_t *am = amax + (long)b * N;
+        int nb = nodes_of(num_nodes, N, b);
+        if (nb < 0 || nb > N) {
+            status = -1;
+            nb = 0;
+        }
         int *acc = malloc(sizeof(int) * (size_t)N);
         int *depth = malloc(sizeof(int) * (size_t)N);
         int sel = -1;
-        for (int i = 0; i < N; ++i) {
+        for (int i = 0; i < nb; ++i) {
             int p = par[i];
             if (p < -1 || p >= i) {
                 status = -1;

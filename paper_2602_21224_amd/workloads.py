@@ -24,6 +24,8 @@ Layouts (all C-contiguous):
   parent   int32              [B, N]           (parent[b, i] in [-1, i-1])
   draft    int32              [B, N]
   logits   float32            [B, N, V]
+  num_nodes int32             [B] or None      (ragged forests: nodes past
+                                                num_nodes[b] are padding)
 """
 from __future__ import annotations
 
@@ -68,6 +70,7 @@ class Workload:
     draft: np.ndarray
     logits: np.ndarray | None
     meta: dict = field(default_factory=dict)
+    num_nodes: np.ndarray | None = None
 
     @property
     def max_pages(self) -> int:
@@ -141,6 +144,22 @@ def tree_topk_expansion(rng: np.random.Generator, branching, keep: int):
             raise AssertionError("pruned tree is not ancestor-closed")
         parent[new] = -1 if p < 0 else relabel[p]
     return parent
+
+
+def fusion_forest(rng: np.random.Generator, primary, resampled, depth_lt: int) -> np.ndarray:
+    """Input of a fused verification (§6.2: the previous round's re-sampled
+    trees are verified together with the next batch): this round's draft tree
+    (root 0) followed by a re-sampled tree with its own root (Alg. 2 roots it
+    at the ground-truth token). `primary` and `resampled` are inclusive node
+    count ranges; both trees are depth-capped random trees."""
+    n1 = int(rng.integers(primary[0], primary[1] + 1))
+    n2 = int(rng.integers(resampled[0], resampled[1] + 1))
+    a = tree_random_depth_capped(rng, n1, depth_lt)
+    if n2 == 0:
+        return a
+    c = tree_random_depth_capped(rng, n2, depth_lt)
+    c = np.where(c >= 0, c + n1, -1).astype(np.int32)
+    return np.concatenate([a, c]).astype(np.int32)
 
 
 def tree_depths(parent: np.ndarray) -> np.ndarray:
@@ -239,14 +258,22 @@ def make_workload(name: str, seed: int, *, B: int, N: int, Hq: int, Hkv: int, D:
                   distinct_siblings: bool = True, poison: bool = False,
                   with_logits: bool = True, forced_path=None) -> Workload:
     """Draw one workload. `kv_len` is an int, a (lo, hi) inclusive range, or
-    an explicit per-sequence list; `parent_fn(rng)` returns one tree."""
+    an explicit per-sequence list; `parent_fn(rng)` returns one tree of at most
+    N nodes. If any tree is shorter than N the batch is ragged: `num_nodes`
+    holds each sequence's node count and every input row of the padding nodes
+    is poisoned (NaN bf16 and fp32 values, out-of-range parents and tokens),
+    so a kernel that reads padding fails visibly."""
     ss = np.random.SeedSequence(seed)
     r_tree, r_len, r_page, r_q, r_kv, r_tree_kv, r_tok, r_logit, r_boost = [
         np.random.default_rng(s) for s in ss.spawn(9)]
 
-    parent = np.stack([np.asarray(parent_fn(r_tree), dtype=np.int32) for _ in range(B)]) \
-        if B else np.zeros((0, N), np.int32)
-    assert parent.shape == (B, N)
+    trees = [np.asarray(parent_fn(r_tree), dtype=np.int32) for _ in range(B)]
+    assert all(1 <= len(t) <= N or (len(t) == 0) for t in trees)
+    counts = np.array([len(t) for t in trees], dtype=np.int32)
+    ragged = bool(B) and bool((counts < N).any())
+    parent = np.full((B, N), -1, dtype=np.int32)
+    for b, t in enumerate(trees):
+        parent[b, :len(t)] = t
 
     if isinstance(kv_len, (int, np.integer)):
         lens = np.full(B, int(kv_len), dtype=np.int32)
@@ -266,23 +293,41 @@ def make_workload(name: str, seed: int, *, B: int, N: int, Hq: int, Hkv: int, D:
     if poison:
         poison_cache_tails(k_cache, v_cache, page_table, lens, P)
 
-    draft = np.stack([draft_tokens(r_tok, parent[b], V, distinct_siblings) for b in range(B)]) \
-        if B else np.zeros((0, N), np.int32)
+    draft = np.zeros((B, N), dtype=np.int32)
+    for b in range(B):
+        n = counts[b]
+        draft[b, :n] = draft_tokens(r_tok, parent[b, :n], V, distinct_siblings)
 
     logits = None
     if with_logits:
         logits = r_logit.standard_normal(size=(B, N, V), dtype=np.float32)
         for b in range(B):
+            n = counts[b]
             if boost_prob > 0.0:
-                boost_logits(r_boost, logits[b], parent[b], draft[b], boost_prob, boost_amount)
+                boost_logits(r_boost, logits[b, :n], parent[b, :n], draft[b, :n], boost_prob,
+                             boost_amount)
             if forced_path is not None:
-                for c in forced_path(parent[b]):
+                for c in forced_path(parent[b, :n]):
                     logits[b, parent[b, c], draft[b, c]] += np.float32(1e9)
 
+    if ragged:
+        for b in range(B):
+            n = counts[b]
+            pad = np.arange(n, N)
+            q[b, n:] = BF16_NAN
+            k_tree[b, n:] = BF16_NAN
+            v_tree[b, n:] = BF16_NAN
+            parent[b, n:] = np.where(pad % 2 == 0, pad + 3, -7)    # outside [-1, i-1]
+            draft[b, n:] = V + 11
+            if logits is not None:
+                logits[b, n:] = np.float32(np.nan)
+
     meta = {"seed": seed, "boost_prob": boost_prob, "boost_amount": boost_amount,
-            "max_depth": [int(tree_depths(parent[b]).max()) for b in range(B)]}
+            "max_depth": [int(tree_depths(parent[b, :counts[b]]).max()) if counts[b] else -1
+                          for b in range(B)]}
     return Workload(name, B, N, Hq, Hkv, D, P, V, q, k_tree, v_tree, k_cache, v_cache,
-                    page_table, lens, parent, draft, logits, meta)
+                    page_table, lens, parent, draft, logits, meta,
+                    counts if ragged else None)
 
 
 # --------------------------------------------------------------------------
@@ -290,6 +335,9 @@ def make_workload(name: str, seed: int, *, B: int, N: int, Hq: int, Hkv: int, D:
 # --------------------------------------------------------------------------
 
 PRESETS = ("tiny", "llama8b_bs1", "llama8b_bs16", "llama70b_bs8", "long_wide_bs4")
+# Ragged forests of a fused verification (this round's tree plus the previous
+# round's re-sampled tree per sequence, padded to N).
+RAGGED_PRESETS = ("llama8b_bs16_fused",)
 
 
 def preset(name: str, *, poison: bool = False, with_logits: bool = True,
@@ -317,6 +365,12 @@ def preset(name: str, *, poison: bool = False, with_logits: bool = True,
                              parent_fn=lambda r: tree_random_depth_capped(r, 128, 10),
                              V=128256, boost_prob=0.5, boost_amount=boost_amount,
                              poison=poison, with_logits=with_logits)
+    if name == "llama8b_bs16_fused":
+        return make_workload(name, 5, B=B or 16, N=64, Hq=32, Hkv=8, D=128,
+                             kv_len=(1024, 4096),
+                             parent_fn=lambda r: fusion_forest(r, (24, 48), (0, 16), 8),
+                             V=128256, boost_prob=0.6, boost_amount=boost_amount,
+                             poison=poison, with_logits=with_logits)
     if name == "long_wide_bs4":
         return make_workload(name, 4, B=B or 4, N=256, Hq=32, Hkv=8, D=128, kv_len=32768,
                              parent_fn=lambda r: tree_random_depth_capped(r, 256, 12,
@@ -337,4 +391,7 @@ PRESET_DOC = {
                     "(depth <= 10), vocab 128256, +3 boost w.p. 0.5",
     "long_wide_bs4": "batch 4, 32/8 heads, head_dim 128, prefix 32768, 256-node trees "
                      "(8 root children, depth <= 12), vocab 128256, +3 boost w.p. 0.4",
+    "llama8b_bs16_fused": "batch 16, 32/8 heads, head_dim 128, prefix U[1024,4096], per "
+                          "sequence a 24-48-node tree plus a 0-16-node re-sampled tree "
+                          "(second root), padded to 64, vocab 128256, seed 5",
 }
