@@ -38,6 +38,14 @@
  *   a re-sampled tree is rooted at, §5.3 / Alg. 2). Roots are always accepted;
  *   several roots form a forest. A node sees itself and its ancestors.
  *
+ * Ragged batches (verification fusion, §6.2: the previous round's re-sampled
+ *   trees are verified together with this round's trees, so sequences carry
+ *   forests of different sizes). The calls that take `num_nodes` accept a
+ *   device array [B] of node counts, or NULL for N nodes everywhere. Sequence
+ *   b then has n_b = num_nodes[b] nodes (clamped to [0, N]); nodes
+ *   n_b .. N-1 are padding: none of their inputs (q, tree K/V, parent, draft
+ *   token, logits row) is read into any result, and work is not spent on them.
+ *
  * Content contract (not checked in the fast path; tv_validate_inputs checks
  * it): parent[b][i] in [-1, i-1]; kv_len[b] >= 0; every page id the prefix
  * and the compacted rows touch lies in [0, num_pages); and
@@ -63,7 +71,7 @@ extern "C" {
 #define TV_API
 #endif
 
-#define TV_ABI_VERSION 1
+#define TV_ABI_VERSION 2
 
 enum tv_status {
     TV_OK = 0,
@@ -107,6 +115,9 @@ TV_API const char *tv_status_string(int status);
  *   page_table  [B, max_pages]             int32
  *   kv_len      [B]                        int32, committed prefix lengths
  *   parent      [B, N]                     int32
+ *   num_nodes   [B]                        int32 node counts, or NULL (see
+ *                                          "Ragged batches"); rows of padding
+ *                                          nodes get out = 0 and lse = -inf
  *   out         [B, N, Hq, D]              bf16, every element written
  *   lse         [B, N, Hq]                 fp32, or NULL
  *   workspace   >= tv_attention_workspace_size(...) bytes of device memory,
@@ -125,8 +136,9 @@ TV_API size_t tv_attention_workspace_size(int B, int N, int Hq, int Hkv, int D);
 TV_API int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree,
                                  const uint16_t *v_tree, const uint16_t *k_cache,
                                  const uint16_t *v_cache, const int32_t *page_table,
-                                 const int32_t *kv_len, const int32_t *parent, int B, int N,
-                                 int Hq, int Hkv, int D, int P, int max_pages, int num_pages,
+                                 const int32_t *kv_len, const int32_t *parent,
+                                 const int32_t *num_nodes, int B, int N, int Hq, int Hkv, int D,
+                                 int P, int max_pages, int num_pages,
                                  int max_kv_len, float scale, uint16_t *out, float *lse,
                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
 
@@ -141,13 +153,18 @@ TV_API int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree,
  *                      draft_tokens[b,i] == argmax_out[b,parent[i]]
  *   sel              = accepted node of greatest depth (root depth 0),
  *                      lowest index on a tie
- *   accept_len[b]    = depth(sel) + 1          (path nodes, root included, >= 1)
+ *   accept_len[b]    = depth(sel) + 1          (path nodes, root included, >= 1
+ *                                              unless the sequence has no nodes)
  *   accept_idx[b,:]  = root .. sel node ids, then -1 up to N
  *   bonus_token[b]   = argmax_out[b, sel]
  *
  *   logits        [B, N, V]  fp32 (V * 4 bytes per row; rows need no alignment)
  *   draft_tokens  [B, N]     int32
  *   parent        [B, N]     int32
+ *   num_nodes     [B]        int32 node counts, or NULL (see "Ragged batches"):
+ *                            only nodes i < n_b take part; argmax_out is -1 for
+ *                            padding nodes; a sequence with n_b == 0 gets
+ *                            accept_len 0, bonus_token -1 and accept_idx all -1
  *   argmax_out    [B, N]     int32
  *   accept_len    [B]        int32
  *   accept_idx    [B, N]     int32
@@ -158,7 +175,8 @@ TV_API int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree,
 TV_API size_t tv_argmax_workspace_size(int B, int N, int V);
 
 TV_API int tree_argmax_accept(const float *logits, const int32_t *draft_tokens,
-                              const int32_t *parent, int B, int N, int V, int32_t *argmax_out,
+                              const int32_t *parent, const int32_t *num_nodes, int B, int N,
+                              int V, int32_t *argmax_out,
                               int32_t *accept_len, int32_t *accept_idx, int32_t *bonus_token,
                               void *workspace, size_t workspace_bytes, hipStream_t stream);
 

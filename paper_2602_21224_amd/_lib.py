@@ -40,11 +40,11 @@ def load():
     lib.tv_status_string.restype = ctypes.c_char_p
     lib.tv_attention_workspace_size.argtypes = [i] * 5
     lib.tv_attention_workspace_size.restype = sz
-    lib.tree_verify_attention.argtypes = [p] * 8 + [i] * 9 + [ctypes.c_float, p, p, p, sz, p]
+    lib.tree_verify_attention.argtypes = [p] * 9 + [i] * 9 + [ctypes.c_float, p, p, p, sz, p]
     lib.tree_verify_attention.restype = i
     lib.tv_argmax_workspace_size.argtypes = [i] * 3
     lib.tv_argmax_workspace_size.restype = sz
-    lib.tree_argmax_accept.argtypes = [p] * 3 + [i] * 3 + [p] * 5 + [sz, p]
+    lib.tree_argmax_accept.argtypes = [p] * 4 + [i] * 3 + [p] * 5 + [sz, p]
     lib.tree_argmax_accept.restype = i
     lib.kv_compact_accepted.argtypes = [p] * 8 + [i] * 7 + [p]
     lib.kv_compact_accepted.restype = i
@@ -98,10 +98,11 @@ def argmax_workspace_size(B, N, V) -> int:
 
 
 def tree_verify_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, *,
-                          max_kv_len: int, scale: float = 0.0, out=None, lse=None,
-                          want_lse: bool = True, workspace=None, stream=None):
+                          max_kv_len: int, num_nodes=None, scale: float = 0.0, out=None,
+                          lse=None, want_lse: bool = True, workspace=None, stream=None):
     """Tree-masked attention of every node over its sequence's paged prefix and
-    its own root path. Returns (out bf16 [B,N,Hq,D], lse fp32 [B,N,Hq] or None)."""
+    its own root path. `num_nodes` (int32 [B], optional) makes the batch ragged.
+    Returns (out bf16 [B,N,Hq,D], lse fp32 [B,N,Hq] or None)."""
     B, N, Hq, D = q.shape
     Hkv = k_tree.shape[2]
     num_pages, P = k_cache.shape[0], k_cache.shape[1]
@@ -114,6 +115,8 @@ def tree_verify_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_le
     _want(page_table, "page_table", (torch.int32,), (B, max_pages))
     _want(kv_len, "kv_len", (torch.int32,), (B,))
     _want(parent, "parent", (torch.int32,), (B, N))
+    if num_nodes is not None:
+        _want(num_nodes, "num_nodes", (torch.int32,), (B,))
     if out is None:
         out = torch.empty((B, N, Hq, D), dtype=torch.bfloat16, device=q.device)
     _want(out, "out", _BF16, (B, N, Hq, D))
@@ -127,21 +130,26 @@ def tree_verify_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_le
     _want(workspace, "workspace", (torch.uint8,))
     st = load().tree_verify_attention(
         _ptr(q), _ptr(k_tree), _ptr(v_tree), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
-        _ptr(kv_len), _ptr(parent), B, N, Hq, Hkv, D, P, max_pages, num_pages, int(max_kv_len),
+        _ptr(kv_len), _ptr(parent), _ptr(num_nodes), B, N, Hq, Hkv, D, P, max_pages, num_pages,
+        int(max_kv_len),
         float(scale), _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "tree_verify_attention")
     return out, lse
 
 
-def tree_argmax_accept(logits, draft_tokens, parent, *, argmax_out=None, accept_len=None,
-                       accept_idx=None, bonus_token=None, workspace=None, stream=None):
+def tree_argmax_accept(logits, draft_tokens, parent, *, num_nodes=None, argmax_out=None,
+                       accept_len=None, accept_idx=None, bonus_token=None, workspace=None,
+                       stream=None):
     """Per-node argmax, greedy longest accepted path and bonus token.
+    `num_nodes` (int32 [B], optional) makes the batch ragged.
     Returns (argmax [B,N], accept_len [B], accept_idx [B,N], bonus [B]) int32."""
     B, N, V = logits.shape
     dev = logits.device
     _want(logits, "logits", (torch.float32,))
     _want(draft_tokens, "draft_tokens", (torch.int32,), (B, N))
     _want(parent, "parent", (torch.int32,), (B, N))
+    if num_nodes is not None:
+        _want(num_nodes, "num_nodes", (torch.int32,), (B,))
     mk = lambda shape: torch.empty(shape, dtype=torch.int32, device=dev)
     argmax_out = mk((B, N)) if argmax_out is None else argmax_out
     accept_len = mk((B,)) if accept_len is None else accept_len
@@ -155,7 +163,7 @@ def tree_argmax_accept(logits, draft_tokens, parent, *, argmax_out=None, accept_
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
     _want(workspace, "workspace", (torch.uint8,))
     st = load().tree_argmax_accept(
-        _ptr(logits), _ptr(draft_tokens), _ptr(parent), B, N, V, _ptr(argmax_out),
+        _ptr(logits), _ptr(draft_tokens), _ptr(parent), _ptr(num_nodes), B, N, V, _ptr(argmax_out),
         _ptr(accept_len), _ptr(accept_idx), _ptr(bonus_token), _ptr(workspace),
         workspace.numel(), _stream(stream))
     _check(st, "tree_argmax_accept")

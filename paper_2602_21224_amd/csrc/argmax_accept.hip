@@ -12,6 +12,11 @@
 // keys into its argmax, then marks the node accepted when every edge of its
 // root path matches, and a block reduction picks the deepest accepted node
 // (lowest index on ties) whose path and argmax give the outputs.
+//
+// Ragged batches (a verification-fusion forest per sequence, §6.2): nodes at
+// or past num_nodes[b] are padding. Their logits rows are not streamed, their
+// argmax is -1 and they take no part in acceptance; a sequence without nodes
+// accepts nothing (length 0, bonus -1).
 #include "tv_internal.h"
 
 namespace tv {
@@ -37,6 +42,12 @@ __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsig
     return a > b ? a : b;
 }
 
+__device__ __forceinline__ int node_count(const int32_t *num_nodes, int b, int N) {
+    if (!num_nodes) return N;
+    const int n = num_nodes[b];
+    return n < 0 ? 0 : (n > N ? N : n);
+}
+
 __device__ __forceinline__ unsigned long long wave_max64(unsigned long long v) {
     #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -49,10 +60,14 @@ __device__ __forceinline__ unsigned long long wave_max64(unsigned long long v) {
 
 // One workgroup per (row, segment). seg_len is a multiple of 4.
 __global__ __launch_bounds__(kArgmaxThreads) void argmax_segments_kernel(
-    const float *__restrict__ logits, int V, int segs, int seg_len,
-    unsigned long long *__restrict__ ws) {
+    const float *__restrict__ logits, const int32_t *__restrict__ num_nodes, int N, int V,
+    int segs, int seg_len, unsigned long long *__restrict__ ws) {
     const size_t row = blockIdx.x;
     const int seg = blockIdx.y;
+    if (num_nodes && (int)(row % N) >= node_count(num_nodes, (int)(row / N), N)) {
+        if (threadIdx.x == 0) ws[row * segs + seg] = 0ull;     // padding node: nothing read
+        return;
+    }
     const int v0 = seg * seg_len;
     const int v1 = min(V, v0 + seg_len);
     const float *x = logits + row * (size_t)V;
@@ -103,17 +118,18 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_segments_kernel(
 
 __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
     const unsigned long long *__restrict__ ws, int segs, const int32_t *__restrict__ draft,
-    const int32_t *__restrict__ parent, int N, int32_t *__restrict__ argmax_out,
-    int32_t *__restrict__ accept_len, int32_t *__restrict__ accept_idx,
-    int32_t *__restrict__ bonus) {
+    const int32_t *__restrict__ parent, const int32_t *__restrict__ num_nodes, int N,
+    int32_t *__restrict__ argmax_out, int32_t *__restrict__ accept_len,
+    int32_t *__restrict__ accept_idx, int32_t *__restrict__ bonus) {
     const int b = blockIdx.x;
     const int i = threadIdx.x;
+    const int nb = node_count(num_nodes, b, N);
     __shared__ int s_par[kMaxNodes];
     __shared__ int s_amax[kMaxNodes];
     __shared__ int s_match[kMaxNodes];
     __shared__ unsigned int s_best[kAcceptThreads / kWave];
 
-    if (i < N) {
+    if (i < nb) {
         const size_t row = (size_t)b * N + i;
         unsigned long long m = 0ull;
         for (int s = 0; s < segs; ++s) m = umax64(m, ws[row * segs + s]);
@@ -124,16 +140,20 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
         if (pi < -1 || pi >= i) pi = -1;                 // contract violation: treat as a root
         s_par[i] = pi;
         accept_idx[row] = -1;
+    } else if (i < N) {
+        const size_t row = (size_t)b * N + i;
+        argmax_out[row] = -1;
+        accept_idx[row] = -1;
     }
     __syncthreads();
     // an edge (parent -> i) matches when i's draft token is the parent's argmax
-    if (i < N) {
+    if (i < nb) {
         const int pi = s_par[i];
         s_match[i] = (pi < 0) || (draft[(size_t)b * N + i] == s_amax[pi]);
     }
     __syncthreads();
     unsigned int key = 0u;              // (depth + 1) << 16 | (0xFFFF - i) for accepted nodes
-    if (i < N) {
+    if (i < nb) {
         int ok = 1, depth = 0;
         for (int j = i; s_par[j] >= 0; j = s_par[j]) {
             ok &= s_match[j];
@@ -150,9 +170,9 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
         #pragma unroll
         for (int w = 1; w < kAcceptThreads / kWave; ++w) k = max(k, s_best[w]);
         const int sel = (int)(0xFFFFu - (k & 0xFFFFu));
-        const int len = (int)(k >> 16);
+        const int len = (int)(k >> 16);          // 0 when the sequence has no nodes
         accept_len[b] = len;
-        bonus[b] = s_amax[sel];
+        bonus[b] = len > 0 ? s_amax[sel] : -1;
         int j = sel;
         for (int d = len - 1; d >= 0; --d) {
             accept_idx[(size_t)b * N + d] = j;
@@ -164,16 +184,17 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
 }  // namespace
 
 hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const int32_t *parent,
-                                int B, int N, int V, int segs, int seg_len, int32_t *argmax_out,
+                                const int32_t *num_nodes, int B, int N, int V, int segs,
+                                int seg_len, int32_t *argmax_out,
                                 int32_t *accept_len, int32_t *accept_idx, int32_t *bonus,
                                 unsigned long long *ws, hipStream_t s) {
     if (B == 0) return hipSuccess;
     hipLaunchKernelGGL(argmax_segments_kernel, dim3(B * N, segs), dim3(kArgmaxThreads), 0, s,
-                       logits, V, segs, seg_len, ws);
+                       logits, num_nodes, N, V, segs, seg_len, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(accept_kernel, dim3(B), dim3(kAcceptThreads), 0, s, ws, segs, draft,
-                       parent, N, argmax_out, accept_len, accept_idx, bonus);
+                       parent, num_nodes, N, argmax_out, accept_len, accept_idx, bonus);
     return hipGetLastError();
 }
 

@@ -50,7 +50,7 @@ namespace {
 
 constexpr int KT = kKeyTile;           // 64 keys per tile
 constexpr int NS = 4;                  // ring stages (a power of two: stage = tile & (NS - 1))
-constexpr int kPageCache = 1024;       // page ids cached in LDS per segment window
+constexpr int kPageCache = 512;        // page ids cached in LDS per segment window
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr float kRescaleSlack = 8.f;   // keep a stale running max while new scores stay within 2^8 of it
@@ -107,6 +107,7 @@ __shared__ int g_jump[2][kMaxNodes];
 __shared__ int g_pages[kPageCache];
 __shared__ int g_cum[kMaxBatchAttn + 1];
 __shared__ int g_len[kMaxBatchAttn];     // clamped prefix length per sequence
+__shared__ unsigned short g_nn[kMaxBatchAttn];   // node count per sequence
 
 __device__ __forceinline__ unsigned lds_addr(const void *p) {
     return (unsigned)(size_t)(const LDS_AS void *)p;
@@ -117,18 +118,38 @@ __device__ __forceinline__ int clamp_len(int L, const AttnParams &p) {
     return L < 0 ? 0 : (L > cap ? cap : L);
 }
 
-__device__ __forceinline__ int tree_tiles_of_block(int rb, const AttnParams &p) {
-    const int last_row = min((rb + 1) * p.rows_per_block, p.rows) - 1;
+// Tree tiles row block rb of a sequence with `rows` query rows must visit.
+__device__ __forceinline__ int tree_tiles_of_block(int rb, int rows, const AttnParams &p) {
+    const int last_row = min((rb + 1) * p.rows_per_block, rows) - 1;
     const int jmax = last_row / p.G + 1;                  // nodes 0 .. jmax-1 may be ancestors
     return (jmax + KT - 1) / KT;
+}
+
+__device__ __forceinline__ int row_blocks_of(int rows, const AttnParams &p) {
+    return (rows + p.rows_per_block - 1) / p.rows_per_block;
+}
+
+// Virtual tiles of one KV head of a sequence with ntp prefix tiles and `rows`
+// query rows: per row block the set-up tiles, the prefix and its tree tiles.
+__device__ __forceinline__ int tiles_per_head(int ntp, int rows, const AttnParams &p) {
+    int t = 0;
+    for (int rb = 0; rb < row_blocks_of(rows, p); ++rb)
+        t += p.setup_tiles + ntp + tree_tiles_of_block(rb, rows, p);
+    return t;
+}
+
+__device__ __forceinline__ int nodes_of(int b, const AttnParams &p) {
+    if (!p.num_nodes) return p.N;
+    const int n = p.num_nodes[b];
+    return n < 0 ? 0 : (n > p.N ? p.N : n);
 }
 
 // Work of sequence b in "virtual" tiles: every unit counts setup_tiles in
 // front of its real tiles (the cost of starting a piece: its set-up and its
 // pipeline fill), so that equal shares of virtual tiles balance the work of
 // workgroups that start new units against those that do not.
-__device__ __forceinline__ int tiles_of_len(int L, const AttnParams &p) {
-    return p.Hkv * (p.row_blocks * ((L + KT - 1) / KT + p.setup_tiles) + p.tree_tiles_all_blocks);
+__device__ __forceinline__ int tiles_of_sequence(int L, int nodes, const AttnParams &p) {
+    return p.Hkv * tiles_per_head((L + KT - 1) / KT, nodes * p.G, p);
 }
 
 // Explicit LDS wait for reads issued through inline assembly; `tie` makes a
@@ -166,9 +187,10 @@ __device__ __forceinline__ void wait_tile_loads(int newer_tiles, int loads_per_t
     else wait_vmcnt<0>();
 }
 
-// Exclusive prefix sum of per-sequence tile counts into g_cum[0..B] and the
-// clamped prefix lengths into g_len[0..B): wave 0 reads kv_len once per lane
-// and scans with cross-lane shifts, one barrier for the whole workgroup.
+// Exclusive prefix sum of per-sequence tile counts into g_cum[0..B], the
+// clamped prefix lengths into g_len[0..B) and the node counts into g_nn:
+// wave 0 reads kv_len (and num_nodes) once per lane and scans with cross-lane
+// shifts, one barrier for the whole workgroup.
 template <int NT>
 __device__ void build_cumulative(const AttnParams &p) {
     if (threadIdx.x < kWave) {
@@ -177,7 +199,8 @@ __device__ void build_cumulative(const AttnParams &p) {
         for (int b0 = 0; b0 < p.B; b0 += kWave) {
             const int b = b0 + lane;
             const int L = b < p.B ? clamp_len(p.kv_len[b], p) : 0;
-            const int t = b < p.B ? tiles_of_len(L, p) : 0;
+            const int nb = b < p.B ? nodes_of(b, p) : 0;
+            const int t = b < p.B ? tiles_of_sequence(L, nb, p) : 0;
             int x = t;                                   // inclusive scan over the wave
             #pragma unroll
             for (int off = 1; off < kWave; off <<= 1) {
@@ -187,6 +210,7 @@ __device__ void build_cumulative(const AttnParams &p) {
             if (b < p.B) {
                 g_cum[b] = carry + x - t;
                 g_len[b] = L;
+                g_nn[b] = (unsigned short)nb;
             }
             carry += __shfl(x, kWave - 1);
         }
@@ -298,7 +322,7 @@ struct TileIssue {
     const char *kc_g, *vc_g;                          // cache base + KV head g
     const char *kt_g, *vt_g;                          // tree row of node 0, KV head g
     unsigned row_bytes, page_bytes;                   // key row of all KV heads; one page
-    int L, ntp;
+    int L, ntp, nodes;
 
     __device__ __forceinline__ void init(int wave_u, int lane, const AttnParams &p) {
         row_bytes = (unsigned)(p.Hkv * D * 2);
@@ -312,9 +336,11 @@ struct TileIssue {
         }
     }
 
-    __device__ __forceinline__ void set_unit(const AttnParams &p, int b, int g, int L_, int ntp_) {
+    __device__ __forceinline__ void set_unit(const AttnParams &p, int b, int g, int L_, int ntp_,
+                                             int nodes_) {
         L = L_;
         ntp = ntp_;
+        nodes = nodes_;
         kc_g = reinterpret_cast<const char *>(p.k_cache + (size_t)g * D);
         vc_g = reinterpret_cast<const char *>(p.v_cache + (size_t)g * D);
         kt_g = reinterpret_cast<const char *>(p.k_tree + ((size_t)b * p.N * p.Hkv + g) * D);
@@ -339,8 +365,9 @@ struct TileIssue {
     }
 
     // Block addresses of tile t. A block with no existing row (past the prefix,
-    // past N, or with an invalid page id) points at tree node 0's row, which is
-    // always readable; its rows are masked later.
+    // past the sequence's nodes, or with an invalid page id) points at tree
+    // node 0's row, which is always readable and finite; its rows are masked
+    // later.
     __device__ __forceinline__ Blocks blocks(const AttnParams &p, int t, int wave_u,
                                              const int (&pg)[LPT]) const {
         Blocks r;
@@ -361,7 +388,7 @@ struct TileIssue {
             #pragma unroll
             for (int i = 0; i < LPT; ++i) {
                 const int j0 = (t - ntp) * KT + (wave_u * LPT + i) * KPB;
-                const int nv = min(max(p.N - j0, 0), KPB);
+                const int nv = min(max(nodes - j0, 0), KPB);
                 const unsigned off = nv > 0 ? (unsigned)j0 * (unsigned)row_bytes : 0u;
                 r.k[i] = kt_g + off;
                 r.v[i] = vt_g + off;
@@ -681,18 +708,20 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         }
         const int b = lo;
         const int L = g_len[b];
+        const int nodes = g_nn[b];
+        const int rows_b = nodes * p.G;                 // this sequence's query rows per KV head
         const int ntp = (L + KT - 1) / KT;
         const int C = p.setup_tiles;
-        const int per_g = p.row_blocks * (ntp + C) + p.tree_tiles_all_blocks;
+        const int per_g = tiles_per_head(ntp, rows_b, p);
         int off = pos - g_cum[b];
         const int g = off / per_g;
         off -= g * per_g;
         int rb = 0;
-        int ulen = ntp + tree_tiles_of_block(0, p);     // real tiles of the unit
+        int ulen = ntp + tree_tiles_of_block(0, rows_b, p);     // real tiles of the unit
         while (off >= C + ulen) {
             off -= C + ulen;
             ++rb;
-            ulen = ntp + tree_tiles_of_block(rb, p);
+            ulen = ntp + tree_tiles_of_block(rb, rows_b, p);
         }
         // this share covers virtual tiles [off, v_end) of the unit; real tile
         // r is virtual tile C + r
@@ -704,7 +733,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             const int wf = share_of(unit_real_start);
             const bool mine = unit_real_start < start && share_of(unit_real_start + ulen - 1) == w;
             *reinterpret_cast<i32x4 *>(p.ws_desc + w * 4) =
-                mine ? i32x4{b, g, rb, wf * 2 + (unit_real_start <= share_start(wf) ? 0 : 1)}
+                mine ? i32x4{b, g, rb | (nodes << 8), wf * 2 + (unit_real_start <= share_start(wf) ? 0 : 1)}
                      : i32x4{-1, 0, 0, 0};
         }
         pos += v_end - off;
@@ -715,7 +744,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
 
         // ---- this wave's 32 query rows: Q fragments stay in registers
         const int row = rb * p.rows_per_block + wave_u * kRowsPerWave + col;
-        const bool row_ok = row < p.rows;
+        const bool row_ok = row < rows_b;
         const int node = row_ok ? row / p.G : 0;
         const int hq = g * p.G + (row_ok ? row % p.G : 0);
         WaveState<D> st;
@@ -795,7 +824,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
 
             // Q (issued above) and the first tiles are in flight together: the
             // first tile wait below also covers Q, which was issued earlier.
-            ld.set_unit(p, b, g, L, ntp);
+            ld.set_unit(p, b, g, L, ntp, nodes);
             {
                 int ids[4][LPT];
                 #pragma unroll
@@ -960,6 +989,20 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             }
         }
     }
+
+    // Rows of padding nodes (at or past a sequence's node count) are not part
+    // of any unit: write them as zeros with lse -inf, a few nodes per workgroup.
+    if (p.num_nodes) {
+        const int chunks = p.Hq * D / 8;             // 16-byte chunks of one node's output
+        for (int idx = w; idx < p.B * p.N; idx += p.num_wg) {
+            const int b = idx / p.N, i = idx - b * p.N;
+            if (i < g_nn[b]) continue;
+            u16x8 *op = reinterpret_cast<u16x8 *>(p.out + ((size_t)b * p.N + i) * p.Hq * D);
+            for (int c = tid; c < chunks; c += NT) op[c] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+            if (p.lse)
+                for (int h = tid; h < p.Hq; h += NT) p.lse[((size_t)b * p.N + i) * p.Hq + h] = kNegInf;
+        }
+    }
 }
 
 // Merge the pieces of every split unit. Block (chunk, h) serves the workgroup
@@ -979,13 +1022,14 @@ __global__ __launch_bounds__(256) void tree_attention_merge_kernel(AttnParams p,
     const i32x4 d = ((const CONST_AS i32x4 *)p.ws_desc)[w];
     const int b = d[0];
     if (b < 0) return;
-    const int g = d[1], rb = d[2], s0 = d[3];
+    const int g = d[1], rb = d[2] & 0xFF, s0 = d[3];
+    const int rows_b = (d[2] >> 8) * p.G;
     const int wf = s0 >> 1;
 
     const int rl = rchunk * kRowsPerWg + threadIdx.x / D8;
     const int d8 = threadIdx.x % D8;
     const int row = rb * p.rows_per_block + rl;
-    if (rl >= p.rows_per_block || row >= p.rows) return;
+    if (rl >= p.rows_per_block || row >= rows_b) return;
 
     float M = kNegInf, den = 0.f;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};

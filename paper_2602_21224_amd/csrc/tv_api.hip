@@ -139,8 +139,9 @@ size_t tv_attention_workspace_size(int B, int N, int Hq, int Hkv, int D) {
 int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
                           const uint16_t *k_cache, const uint16_t *v_cache,
                           const int32_t *page_table, const int32_t *kv_len, const int32_t *parent,
-                          int B, int N, int Hq, int Hkv, int D, int P, int max_pages,
-                          int num_pages, int max_kv_len, float scale, uint16_t *out, float *lse,
+                          const int32_t *num_nodes, int B, int N, int Hq, int Hkv, int D, int P,
+                          int max_pages, int num_pages, int max_kv_len, float scale, uint16_t *out,
+                          float *lse,
                           void *workspace, size_t workspace_bytes, hipStream_t stream) {
     if (!attn_shape_ok(B, N, Hq, Hkv, D)) return TV_ERR_SHAPE;
     if (!pow2(P) || P > 256 || max_pages < 1 || num_pages < 1 || max_kv_len < 0)
@@ -176,17 +177,16 @@ int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
 
     tv::AttnParams p;
     p.q = q; p.k_tree = k_tree; p.v_tree = v_tree; p.k_cache = k_cache; p.v_cache = v_cache;
-    p.page_table = page_table; p.kv_len = kv_len; p.parent = parent;
+    p.page_table = page_table; p.kv_len = kv_len; p.parent = parent; p.num_nodes = num_nodes;
     p.out = out; p.lse = lse;
     char *base = static_cast<char *>(workspace);
     p.ws_o = reinterpret_cast<uint16_t *>(base);
     p.ws_ml = reinterpret_cast<float *>(base + ws.o_bytes);
     p.ws_desc = reinterpret_cast<int32_t *>(base + ws.o_bytes + ws.ml_bytes);
-    p.B = B; p.N = N; p.Hq = Hq; p.Hkv = Hkv; p.G = s.G; p.rows = s.rows;
+    p.B = B; p.N = N; p.Hq = Hq; p.Hkv = Hkv; p.G = s.G;
     p.P = P; p.p_shift = __builtin_ctz((unsigned)P);
     p.max_pages = max_pages; p.num_pages = num_pages;
-    p.rows_per_block = s.rows_per_block; p.row_blocks = s.row_blocks;
-    p.tree_tiles_all_blocks = s.tree_tiles_all;
+    p.rows_per_block = s.rows_per_block;
     p.setup_tiles = kSetupTiles;
     p.small_pages = P < 1024 / (2 * D) ? 1 : 0;
     p.num_wg = (int)num_wg;
@@ -205,7 +205,8 @@ size_t tv_argmax_workspace_size(int B, int N, int V) {
 }
 
 int tree_argmax_accept(const float *logits, const int32_t *draft_tokens, const int32_t *parent,
-                       int B, int N, int V, int32_t *argmax_out, int32_t *accept_len,
+                       const int32_t *num_nodes, int B, int N, int V, int32_t *argmax_out,
+                       int32_t *accept_len,
                        int32_t *accept_idx, int32_t *bonus_token, void *workspace,
                        size_t workspace_bytes, hipStream_t stream) {
     if (B < 0 || B > 65535 || N < 1 || N > tv::kMaxNodes || V < 1) return TV_ERR_SHAPE;
@@ -220,7 +221,8 @@ int tree_argmax_accept(const float *logits, const int32_t *draft_tokens, const i
     int segs = 1, seg_len = 4;
     argmax_plan(B, N, V, &segs, &seg_len);
     const hipError_t e = tv::launch_argmax_accept(
-        logits, draft_tokens, parent, B, N, V, segs, seg_len, argmax_out, accept_len, accept_idx,
+        logits, draft_tokens, parent, num_nodes, B, N, V, segs, seg_len, argmax_out, accept_len,
+        accept_idx,
         bonus_token, static_cast<unsigned long long *>(workspace), stream);
     return e == hipSuccess ? TV_OK : TV_ERR_HIP;
 }

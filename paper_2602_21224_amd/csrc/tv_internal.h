@@ -27,15 +27,15 @@ constexpr int kMaxBatchAttn = 1024;
 struct AttnParams {
     const uint16_t *q, *k_tree, *v_tree, *k_cache, *v_cache;
     const int32_t *page_table, *kv_len, *parent;
+    const int32_t *num_nodes;   // [B] node count per sequence, or null (N each)
     uint16_t *out;
     float *lse;
     uint16_t *ws_o;    // [num_wg * 2][rows_per_block][D] bf16 partial outputs (normalised)
     float *ws_ml;      // [num_wg * 2][rows_per_block][2] partial (max, sum)
     int32_t *ws_desc;  // [num_wg][4] per workgroup: the split unit it finishes (b, g, rb, first slot), b < 0 if none
-    int B, N, Hq, Hkv, G, rows, P, p_shift, max_pages, num_pages;
-    int rows_per_block, row_blocks;
+    int B, N, Hq, Hkv, G, P, p_shift, max_pages, num_pages;
+    int rows_per_block;          // query rows of one unit (the workgroup's waves x 32)
     int small_pages;             // pages shorter than one 1 KB load block of keys
-    int tree_tiles_all_blocks;   // sum over row blocks of the tree tiles each needs
     int setup_tiles;             // cost of starting a unit piece, in tiles (work balance)
     int num_wg;
     float scale_log2;            // softmax scale * log2(e)
@@ -55,7 +55,8 @@ __device__ __forceinline__ int xcd_contiguous_id(int hw_id, int n) {
 // Host-side launchers (defined next to their kernels).
 hipError_t launch_tree_attention(const AttnParams &p, int head_dim, int waves, hipStream_t s);
 hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const int32_t *parent,
-                                int B, int N, int V, int segs, int seg_len, int32_t *argmax_out,
+                                const int32_t *num_nodes, int B, int N, int V, int segs,
+                                int seg_len, int32_t *argmax_out,
                                 int32_t *accept_len, int32_t *accept_idx, int32_t *bonus,
                                 unsigned long long *ws, hipStream_t s);
 hipError_t launch_kv_compact(const uint16_t *k_tree, const uint16_t *v_tree, uint16_t *k_cache,

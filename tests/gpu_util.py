@@ -33,14 +33,16 @@ def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
 def upload(w):
     return dict(q=dev_bf16(w.q), k_tree=dev_bf16(w.k_tree), v_tree=dev_bf16(w.v_tree),
                 k_cache=dev_bf16(w.k_cache), v_cache=dev_bf16(w.v_cache),
-                page_table=dev(w.page_table), kv_len=dev(w.kv_len), parent=dev(w.parent))
+                page_table=dev(w.page_table), kv_len=dev(w.kv_len), parent=dev(w.parent),
+                num_nodes=None if w.num_nodes is None else dev(w.num_nodes))
 
 
 def gpu_attention(T, w, scale=0.0, d=None):
     d = d or upload(w)
     out, lse = T.tree_verify_attention(d["q"], d["k_tree"], d["v_tree"], d["k_cache"],
                                        d["v_cache"], d["page_table"], d["kv_len"], d["parent"],
-                                       max_kv_len=w.max_kv_len, scale=scale)
+                                       max_kv_len=w.max_kv_len, scale=scale,
+                                       num_nodes=d["num_nodes"])
     torch.cuda.synchronize()
     return bf16_to_f64(out), lse.cpu().numpy().astype(np.float64)
 

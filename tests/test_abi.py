@@ -47,7 +47,7 @@ def test_only_declared_symbols_are_exported():
 
 
 def test_status_strings(lib):
-    assert lib.tv_abi_version() == 1
+    assert lib.tv_abi_version() == 2
     for code in range(0, -7, -1):
         assert lib.tv_status_string(code)
     assert lib.tv_status_string(-99) == b"unknown status"
@@ -60,7 +60,8 @@ STREAM = ctypes.c_void_p(0)
 
 def attn(lib, **kw):
     a = dict(q=FAKE, k_tree=FAKE, v_tree=FAKE, k_cache=FAKE, v_cache=FAKE, page_table=FAKE,
-             kv_len=FAKE, parent=FAKE, B=2, N=8, Hq=8, Hkv=2, D=128, P=16, max_pages=4,
+             kv_len=FAKE, parent=FAKE, num_nodes=NULL, B=2, N=8, Hq=8, Hkv=2, D=128, P=16,
+             max_pages=4,
              num_pages=8, max_kv_len=32, scale=0.0, out=FAKE, lse=NULL, ws=FAKE,
              ws_bytes=1 << 40)
     a.update(kw)
@@ -80,6 +81,7 @@ def test_attention_argument_checks(lib):
     assert attn(lib, q=ctypes.c_void_p(0x10008)) == -3
     # well-formed on a machine without a GPU: stops at the device check, launches nothing
     assert attn(lib) in (-4, -6)
+    assert attn(lib, num_nodes=FAKE) in (-4, -6)       # node counts are optional
 
 
 def test_workspace_size_is_monotone_and_rejects_bad_shapes(lib):
@@ -92,7 +94,8 @@ def test_workspace_size_is_monotone_and_rejects_bad_shapes(lib):
 
 
 def test_accept_and_compact_argument_checks(lib):
-    acc = lambda **kw: lib.tree_argmax_accept(*{**dict(l=FAKE, d=FAKE, p=FAKE, B=2, N=4, V=100,
+    acc = lambda **kw: lib.tree_argmax_accept(*{**dict(l=FAKE, d=FAKE, p=FAKE, nn=NULL, B=2,
+                                                        N=4, V=100,
                                                         a=FAKE, al=FAKE, ai=FAKE, b=FAKE,
                                                         ws=FAKE, wsb=1 << 30), **kw}.values(),
                                               STREAM)

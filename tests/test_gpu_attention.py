@@ -31,7 +31,15 @@ def full_compare(oracle_mod, T, w, label, scale=0.0):
           f"kv_len={w.kv_len.tolist()[:8]}", flush=True)
     got, glse = U.gpu_attention(T, w, scale=scale)
     want, wlse = oracle_mod.tree_attention(w.q, w.k_tree, w.v_tree, w.k_cache, w.v_cache,
-                                           w.page_table, w.kv_len, w.parent, scale=scale)
+                                           w.page_table, w.kv_len, w.parent, scale=scale,
+                                           num_nodes=w.num_nodes)
+    if w.num_nodes is not None:
+        # padding rows are exact: zeros, lse -inf; compare the rest numerically
+        for b in range(w.B):
+            n = int(w.num_nodes[b])
+            assert (got[b, n:] == 0).all() and np.isneginf(glse[b, n:]).all(), (label, b)
+            glse[b, n:] = 0.0
+            wlse[b, n:] = 0.0
     U.assert_attention_close(got, want, glse, wlse, label)
 
 
