@@ -8,8 +8,9 @@ one HIP stream. Inputs are resident in HBM before timing starts; consecutive
 steps rotate over several copies of the inputs (more than 1 GB apart) so no
 step finds its data in the 256 MB Infinity Cache.
 
-Prints ONE JSON line. `value` is verified tree-tokens per second (B * N tree
-nodes verified per step / wall time per step). `roofline` describes the
+Prints ONE JSON line. `value` is verified tree-tokens per second (tree nodes
+verified per step / wall time per step; B * N, or the real nodes of a ragged
+verification-fusion batch). `roofline` describes the
 kernel call that takes the most time; `roofline_attention` the attention
 call. `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
 """
@@ -42,20 +43,34 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
+def real_nodes(w) -> np.ndarray:
+    """Nodes per sequence that the step verifies (all N unless the batch is ragged)."""
+    if w.num_nodes is None:
+        return np.full(w.B, w.N, dtype=np.int64)
+    return np.clip(w.num_nodes.astype(np.int64), 0, w.N)
+
+
 def algorithmic(w):
-    """Bytes (and FLOP) the method itself must move (and do) per call."""
+    """Bytes (and FLOP) the method itself must move (and do) per call. Padding
+    nodes of a ragged batch are not counted: only real nodes are verified."""
     from paper_2602_21224_amd.workloads import tree_depths
     L = w.kv_len.astype(np.int64)
+    nn = real_nodes(w)
+    R = int(nn.sum())
+    live = nn > 0                                             # sequences with work
     row = w.Hkv * w.D * 2                                     # one K or V row, bf16
-    anc = sum(int((tree_depths(w.parent[b]) + 1).sum()) for b in range(w.B))
-    pages_used = int(sum((int(l) + w.P - 1) // w.P for l in L))
-    attn_bytes = (int(L.sum()) * row * 2                      # prefix K + V
-                  + w.B * w.N * row * 2                       # tree K + V
-                  + 2 * w.B * w.N * w.Hq * w.D * 2            # q in, out
-                  + w.B * w.N * w.Hq * 4                      # lse out
-                  + pages_used * 4 + w.B * w.N * 4 + w.B * 4)  # page ids, parent, kv_len
-    attn_flop = 4 * w.N * w.Hq * w.D * int(L.sum()) + 4 * w.Hq * w.D * anc
-    accept_bytes = w.B * w.N * w.V * 4 + 3 * w.B * w.N * 4 + w.B * w.N * 4 + 2 * w.B * 4
+    anc = sum(int((tree_depths(w.parent[b][:nn[b]]) + 1).sum()) for b in range(w.B) if nn[b])
+    pages_used = int(sum((int(l) + w.P - 1) // w.P for l in L[live]))
+    attn_bytes = (int(L[live].sum()) * row * 2                # prefix K + V
+                  + R * row * 2                               # tree K + V
+                  + 2 * R * w.Hq * w.D * 2                    # q in, out
+                  + R * w.Hq * 4                              # lse out
+                  + pages_used * 4 + R * 4 + w.B * 4)         # page ids, parent, kv_len
+    attn_flop = 4 * w.Hq * w.D * int((nn * L).sum()) + 4 * w.Hq * w.D * anc
+    accept_bytes = R * w.V * 4 + 3 * R * 4 + R * 4 + 2 * w.B * 4
+    if w.num_nodes is not None:
+        attn_bytes += w.B * 4                                 # node counts
+        accept_bytes += w.B * 4
     return attn_bytes, attn_flop, accept_bytes
 
 
@@ -147,19 +162,21 @@ def cpu_baseline(w, sample_b: int, min_seconds: float = 10.0):
     """The fp64 CPU oracle on the first `sample_b` sequences of the same workload."""
     import oracle
     sl = slice(0, sample_b)
+    nn = None if w.num_nodes is None else w.num_nodes[sl]
     reps, t0 = 0, time.perf_counter()
     while True:      # repeat the sample until about min_seconds of CPU work
         oracle.tree_attention(w.q[sl], w.k_tree[sl], w.v_tree[sl], w.k_cache, w.v_cache,
-                              w.page_table[sl], w.kv_len[sl], w.parent[sl])
+                              w.page_table[sl], w.kv_len[sl], w.parent[sl], num_nodes=nn)
         a = oracle.argmax(w.logits[sl])
-        alen, aidx, _ = oracle.accept(w.draft[sl], w.parent[sl], a)
+        alen, aidx, _ = oracle.accept(w.draft[sl], w.parent[sl], a, num_nodes=nn)
         oracle.kv_compact(w.k_tree[sl], w.v_tree[sl], w.k_cache, w.v_cache, w.page_table[sl],
                           w.kv_len[sl], aidx, alen)
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds or reps >= 50:
             break
-    return {"value": round(reps * sample_b * w.N / dt, 2), "unit": "verified tree-tokens/s",
+    tokens = int(real_nodes(w)[sl].sum())
+    return {"value": round(reps * tokens / dt, 2), "unit": "verified tree-tokens/s",
             "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{sample_b} of {w.B} sequences of the same workload, {reps} passes "
                       f"(fp64 C, OpenMP), {dt:.2f} s"}
@@ -221,6 +238,8 @@ def main():
                 k_cache=up(w.k_cache, True), v_cache=up(w.v_cache, True),
                 page_table=up(w.page_table), kv_len=up(w.kv_len), parent=up(w.parent),
                 draft=up(w.draft), logits=up(w.logits))
+    if w.num_nodes is not None:
+        base["num_nodes"] = up(w.num_nodes)
     copies = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(args.copies - 1)]
     ws_attn = torch.empty(T.attention_workspace_size(w.B, w.N, w.Hq, w.Hkv, w.D),
                           dtype=torch.uint8, device=dev)
@@ -240,11 +259,11 @@ def main():
         T.tree_verify_attention(c["q"], c["k_tree"], c["v_tree"], c["k_cache"], c["v_cache"],
                                 c["page_table"], c["kv_len"], c["parent"],
                                 max_kv_len=w.max_kv_len, out=o["out"], lse=o["lse"],
-                                workspace=ws_attn)
+                                workspace=ws_attn, num_nodes=c.get("num_nodes"))
         if ev: ev[1].record(stream)
         T.tree_argmax_accept(c["logits"], c["draft"], c["parent"], argmax_out=o["amax"],
                              accept_len=o["alen"], accept_idx=o["aidx"], bonus_token=o["bonus"],
-                             workspace=ws_acc)
+                             workspace=ws_acc, num_nodes=c.get("num_nodes"))
         if ev: ev[2].record(stream)
         T.kv_compact_accepted(c["k_tree"], c["v_tree"], c["k_cache"], c["v_cache"],
                               c["page_table"], c["kv_len"], o["aidx"], o["alen"])
@@ -266,7 +285,7 @@ def main():
     t_acc = np.array([e[1].elapsed_time(e[2]) for e in evs]) * 1e-3
     t_cmp = np.array([e[2].elapsed_time(e[3]) for e in evs]) * 1e-3
     ms_per_step = wall / args.steps * 1e3
-    tokens = w.B * w.N
+    tokens = int(real_nodes(w).sum())
     value = tokens / (wall / args.steps)
 
     alen = outs[0]["alen"].cpu().numpy()
@@ -303,7 +322,8 @@ def main():
                    "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.D, "page_size": w.P,
                    "vocab": w.V, "kv_len_sum": int(w.kv_len.sum()),
                    "kv_len_range": [int(w.kv_len.min()), int(w.kv_len.max())],
-                   "input_copies_rotated": len(copies)},
+                   "input_copies_rotated": len(copies),
+                   "verified_nodes_per_step": tokens},
         "roofline": dominant,
         "roofline_attention": r_attn,
         "step_breakdown_us": {"attention": round(t_attn.mean() * 1e6, 2),
