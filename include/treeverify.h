@@ -210,12 +210,17 @@ TV_API int kv_compact_accepted(const uint16_t *k_tree, const uint16_t *v_tree, u
  * Checks the content contract on the device and writes a bit set to
  * *status_word (device int32): bit 0 parent out of [-1, i-1]; bit 1 negative
  * kv_len; bit 2 a prefix or compaction page index beyond max_pages; bit 3 a
- * page id the prefix or the N tree rows would use outside [0, num_pages).
- * 0 means the inputs satisfy the contract for up to N compacted rows.
+ * page id the prefix or the tree rows would use outside [0, num_pages); bit 4
+ * a node count outside [0, N]. 0 means the inputs satisfy the contract for up
+ * to n_b compacted rows per sequence.
+ * num_nodes: device [B] node counts of a ragged batch, or NULL (N everywhere).
+ * With it, parents of padding nodes are not checked, and a sequence without
+ * nodes has no pages checked (no call reads its prefix).
  * ------------------------------------------------------------------------ */
 TV_API int tv_validate_inputs(const int32_t *page_table, const int32_t *kv_len,
-                              const int32_t *parent, int B, int N, int P, int max_pages,
-                              int num_pages, int32_t *status_word, hipStream_t stream);
+                              const int32_t *parent, const int32_t *num_nodes, int B, int N,
+                              int P, int max_pages, int num_pages, int32_t *status_word,
+                              hipStream_t stream);
 
 #ifdef __cplusplus
 }

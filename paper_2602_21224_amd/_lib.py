@@ -48,7 +48,7 @@ def load():
     lib.tree_argmax_accept.restype = i
     lib.kv_compact_accepted.argtypes = [p] * 8 + [i] * 7 + [p]
     lib.kv_compact_accepted.restype = i
-    lib.tv_validate_inputs.argtypes = [p] * 3 + [i] * 5 + [p, p]
+    lib.tv_validate_inputs.argtypes = [p] * 4 + [i] * 5 + [p, p]
     lib.tv_validate_inputs.restype = i
     _lib = lib
     return lib
@@ -192,15 +192,18 @@ def kv_compact_accepted(k_tree, v_tree, k_cache, v_cache, page_table, kv_len, ac
     return k_cache, v_cache
 
 
-def tv_validate_inputs(page_table, kv_len, parent, *, P: int, num_pages: int, stream=None):
+def tv_validate_inputs(page_table, kv_len, parent, *, P: int, num_pages: int, num_nodes=None,
+                       stream=None):
     """Device-side contract check; returns the status bit set as a 1-element int32 tensor."""
     B, N = parent.shape
     max_pages = page_table.shape[1]
     _want(page_table, "page_table", (torch.int32,), (B, max_pages))
     _want(kv_len, "kv_len", (torch.int32,), (B,))
     _want(parent, "parent", (torch.int32,), (B, N))
+    if num_nodes is not None:
+        _want(num_nodes, "num_nodes", (torch.int32,), (B,))
     word = torch.empty(1, dtype=torch.int32, device=parent.device)
-    st = load().tv_validate_inputs(_ptr(page_table), _ptr(kv_len), _ptr(parent), B, N, P,
+    st = load().tv_validate_inputs(_ptr(page_table), _ptr(kv_len), _ptr(parent), _ptr(num_nodes), B, N, P,
                                    max_pages, num_pages, _ptr(word), _stream(stream))
     _check(st, "tv_validate_inputs")
     return word

@@ -43,21 +43,31 @@ __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(
 
 __global__ __launch_bounds__(256) void validate_kernel(
     const int32_t *__restrict__ page_table, const int32_t *__restrict__ kv_len,
-    const int32_t *__restrict__ parent, int B, int N, int P, int max_pages, int num_pages,
-    int32_t *__restrict__ status_word) {
+    const int32_t *__restrict__ parent, const int32_t *__restrict__ num_nodes, int B, int N,
+    int P, int max_pages, int num_pages, int32_t *__restrict__ status_word) {
     __shared__ int flags;
     if (threadIdx.x == 0) flags = 0;
     __syncthreads();
     int f = 0;
     for (long idx = threadIdx.x; idx < (long)B * N; idx += blockDim.x) {
-        const int i = (int)(idx % N);
+        const int b = (int)(idx / N), i = (int)(idx % N);
+        if (num_nodes) {
+            const int nb = num_nodes[b];
+            if (nb < 0 || nb > N) { f |= 16; continue; }
+            if (i >= nb) continue;                          // padding node: never read
+        }
         const int pi = parent[idx];
         if (pi < -1 || pi >= i) f |= 1;
     }
     for (int b = threadIdx.x; b < B; b += blockDim.x) {
         const int L = kv_len[b];
         if (L < 0) { f |= 2; continue; }
-        const long need = ((long)L + N + P - 1) / P;      // prefix plus up to N compacted rows
+        int nb = N;
+        if (num_nodes) {
+            nb = num_nodes[b];
+            if (nb <= 0 || nb > N) continue;                // no pages are touched (or bit 4)
+        }
+        const long need = ((long)L + nb + P - 1) / P;     // prefix plus up to nb compacted rows
         if (need > max_pages) f |= 4;
         const long upto = need < max_pages ? need : max_pages;
         for (long k = 0; k < upto; ++k) {
@@ -85,10 +95,10 @@ hipError_t launch_kv_compact(const uint16_t *k_tree, const uint16_t *v_tree, uin
 }
 
 hipError_t launch_validate(const int32_t *page_table, const int32_t *kv_len,
-                           const int32_t *parent, int B, int N, int P, int max_pages,
-                           int num_pages, int32_t *status_word, hipStream_t s) {
-    hipLaunchKernelGGL(validate_kernel, dim3(1), dim3(256), 0, s, page_table, kv_len, parent, B, N,
-                       P, max_pages, num_pages, status_word);
+                           const int32_t *parent, const int32_t *num_nodes, int B, int N, int P,
+                           int max_pages, int num_pages, int32_t *status_word, hipStream_t s) {
+    hipLaunchKernelGGL(validate_kernel, dim3(1), dim3(256), 0, s, page_table, kv_len, parent,
+                       num_nodes, B, N, P, max_pages, num_pages, status_word);
     return hipGetLastError();
 }
 

@@ -248,14 +248,14 @@ int kv_compact_accepted(const uint16_t *k_tree, const uint16_t *v_tree, uint16_t
 }
 
 int tv_validate_inputs(const int32_t *page_table, const int32_t *kv_len, const int32_t *parent,
-                       int B, int N, int P, int max_pages, int num_pages, int32_t *status_word,
-                       hipStream_t stream) {
+                       const int32_t *num_nodes, int B, int N, int P, int max_pages,
+                       int num_pages, int32_t *status_word, hipStream_t stream) {
     if (B < 0 || N < 1 || N > tv::kMaxNodes || !pow2(P) || max_pages < 1 || num_pages < 1)
         return TV_ERR_SHAPE;
     if (!status_word || (B > 0 && (!page_table || !kv_len || !parent))) return TV_ERR_NULL;
     if (!device_ok()) return TV_ERR_DEVICE;
-    const hipError_t e = tv::launch_validate(page_table, kv_len, parent, B, N, P, max_pages,
-                                             num_pages, status_word, stream);
+    const hipError_t e = tv::launch_validate(page_table, kv_len, parent, num_nodes, B, N, P,
+                                             max_pages, num_pages, status_word, stream);
     return e == hipSuccess ? TV_OK : TV_ERR_HIP;
 }
 

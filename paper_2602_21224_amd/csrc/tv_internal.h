@@ -64,7 +64,7 @@ hipError_t launch_kv_compact(const uint16_t *k_tree, const uint16_t *v_tree, uin
                              const int32_t *accept_idx, const int32_t *accept_len, int B, int N,
                              int Hkv, int D, int P, int max_pages, int num_pages, hipStream_t s);
 hipError_t launch_validate(const int32_t *page_table, const int32_t *kv_len,
-                           const int32_t *parent, int B, int N, int P, int max_pages,
-                           int num_pages, int32_t *status_word, hipStream_t s);
+                           const int32_t *parent, const int32_t *num_nodes, int B, int N, int P,
+                           int max_pages, int num_pages, int32_t *status_word, hipStream_t s);
 
 }  // namespace tv

@@ -129,3 +129,26 @@ def test_ragged_argmax_accept_and_compaction(oracle_mod):
                                    w.kv_len, aidx, alen)
     assert np.array_equal(kc.view(torch.int16).cpu().numpy().view(np.uint16), wk)
     assert np.array_equal(vc.view(torch.int16).cpu().numpy().view(np.uint16), wv)
+
+
+def test_validate_ragged():
+    """The contract check skips padding (whose parents are poisoned) only when
+    it is given the node counts, and flags counts outside [0, N]."""
+    T = U.require_gpu()
+    w = forest_wl(41, B=6, N=40, Hq=8, Hkv=2, D=64, L=np.array([0, 17, 64, 5, 300, 33]))
+    print(f"case validate: nodes={w.num_nodes.tolist()}", flush=True)
+    pt, kl, par = U.dev(w.page_table), U.dev(w.kv_len), U.dev(w.parent)
+    ok = T.tv_validate_inputs(pt, kl, par, P=w.P, num_pages=w.num_pages,
+                              num_nodes=U.dev(w.num_nodes))
+    assert int(ok.item()) == 0
+    assert (w.num_nodes < w.N).any() and w.num_nodes.max() >= 1
+    dense = T.tv_validate_inputs(pt, kl, par, P=w.P, num_pages=w.num_pages)
+    assert int(dense.item()) & 1                   # padding parents point forward
+    bad_nn = w.num_nodes.copy(); bad_nn[2] = w.N + 1
+    st = T.tv_validate_inputs(pt, kl, par, P=w.P, num_pages=w.num_pages, num_nodes=U.dev(bad_nn))
+    assert int(st.item()) == 16
+    b = int(np.argmax(w.num_nodes))
+    bad_par = w.parent.copy(); bad_par[b, w.num_nodes[b] - 1] = w.num_nodes[b] + 2
+    st = T.tv_validate_inputs(pt, kl, U.dev(bad_par), P=w.P, num_pages=w.num_pages,
+                              num_nodes=U.dev(w.num_nodes))
+    assert int(st.item()) == 1
