@@ -19,7 +19,7 @@
 //     output in bf16) that a second kernel merges with the usual log-sum-exp
 //     rescaling.
 //   * K and V tiles stream from HBM straight into a 4-stage LDS ring with
-//     global_load_lds_dwordx4 (no register staging), three tiles ahead of the
+//     global_load_lds_dwordx4 (no register staging), two tiles ahead of the
 //     one being computed. Each 256-byte row is stored with its 16-byte chunks
 //     XOR-swizzled by the key index, so the MFMA operand reads below are free
 //     of bank conflicts. Keys past the prefix, and tree slots past N, load a
@@ -36,9 +36,9 @@
 //     the fragments they produce, and ring hand-off is s_waitcnt vmcnt(n) +
 //     s_barrier, so the compiler never inserts a blanket wait for the
 //     in-flight tile loads.
-//   * Tree visibility is a per-node ancestor bit set (256 bits) built in LDS by
-//     pointer doubling over the parent links; a masked score is replaced by -inf
-//     (selected, never added).
+//   * Tree visibility is a per-node ancestor bit set (256 bits) in LDS, built
+//     by one wave with pointer doubling over the parent links while the first
+//     tiles load; a masked score is replaced by -inf (selected, never added).
 #include "tv_internal.h"
 
 namespace tv {
@@ -102,7 +102,6 @@ __device__ __forceinline__ float halves_sum(float x) {
 __shared__ __attribute__((aligned(1024))) unsigned char g_ring[NS * Geo<128>::kStageBytes];
 __shared__ unsigned long long g_anc[kMaxNodes][4];
 __shared__ unsigned long long g_anc_alt[kMaxNodes][4];
-__shared__ int g_par[kMaxNodes];
 __shared__ int g_jump[2][kMaxNodes];
 __shared__ int g_pages[kPageCache];
 __shared__ int g_cum[kMaxBatchAttn + 1];
@@ -219,82 +218,115 @@ __device__ void build_cumulative(const AttnParams &p) {
     __syncthreads();
 }
 
-// Segment set-up, part 1: page ids of pages [first, first + kPageCache) of
-// sequence b (as far as it has them) into g_pages, and the parent links of
-// sequence b into g_par. All loads are issued before any is waited for.
+// Piece set-up for pages shorter than a load block: page ids of pages
+// [first, first + kPageCache) of sequence b (as far as it has them) into
+// g_pages; all loads are issued before any is waited for.
 template <int NT>
-__device__ void load_pages_and_parents(const AttnParams &p, int b, int first, int npages,
-                                       bool want_pages, bool want_parents) {
+__device__ void load_pages(const AttnParams &p, int b, int first, int npages) {
     constexpr int PPT = (kPageCache + NT - 1) / NT;
     const int tid = threadIdx.x;
-    const int n = want_pages ? min(kPageCache, npages - first) : 0;
+    const int n = min(kPageCache, npages - first);
     int pg[PPT];
     #pragma unroll
     for (int k = 0; k < PPT; ++k) {
         const int i = tid + k * NT;
         pg[k] = i < n ? p.page_table[(size_t)b * p.max_pages + first + i] : -1;
     }
-    int par[(kMaxNodes + NT - 1) / NT];
-    #pragma unroll
-    for (int k = 0; k < (kMaxNodes + NT - 1) / NT; ++k) {
-        const int i = tid + k * NT;
-        par[k] = (want_parents && i < p.N) ? p.parent[(size_t)b * p.N + i] : -1;
-    }
     #pragma unroll
     for (int k = 0; k < PPT; ++k) {
         const int i = tid + k * NT;
         if (i < n) g_pages[i] = (pg[k] >= 0 && pg[k] < p.num_pages) ? pg[k] : -1;
     }
-    #pragma unroll
-    for (int k = 0; k < (kMaxNodes + NT - 1) / NT; ++k) {
-        const int i = tid + k * NT;
-        if (want_parents && i < p.N) {
-            const int pi = par[k];
-            g_par[i] = (pi < -1 || pi >= i) ? -1 : pi;   // contract violation: treat as a root
-        }
-    }
     __syncthreads();
 }
 
-// Segment set-up, part 2: ancestor bit sets of the N nodes (from g_par) by
-// pointer doubling: after round k a node's set holds every ancestor within
-// distance < 2^k. Runs while the first tiles are in flight. Result in g_anc.
-template <int NT>
-__device__ void build_ancestor_masks(const AttnParams &p) {
-    const int tid = threadIdx.x;
-    for (int i = tid; i < p.N; i += NT) {
-        #pragma unroll
-        for (int w = 0; w < 4; ++w) g_anc[i][w] = (w == (i >> 6)) ? (1ull << (i & 63)) : 0ull;
-        g_jump[0][i] = g_par[i];
+// Ancestor sets of a tree of at most 64 nodes, by one wave and without
+// barriers: lane i holds node i's set (one 64-bit word, reflexive) and the
+// ancestor 2^k steps up; each round ORs in that ancestor's set and jumps
+// twice as far (cross-lane reads see the values of the previous round), until
+// no lane has an ancestor left. The caller's next workgroup barrier publishes
+// g_anc.
+__device__ void build_ancestor_masks_wave(const AttnParams &p, int b) {
+    const int lane = threadIdx.x & (kWave - 1);
+    int j = -1;
+    if (lane < p.N) {
+        const int pi = p.parent[(size_t)b * p.N + lane];
+        j = (pi < -1 || pi >= lane) ? -1 : pi;        // contract violation: treat as a root
     }
-    __syncthreads();
+    unsigned long long anc = lane < p.N ? (1ull << lane) : 0ull;
+    while (__any(j >= 0)) {
+        const int src = j >= 0 ? j : lane;
+        const unsigned lo = (unsigned)__shfl((int)(unsigned)anc, src);
+        const unsigned hi = (unsigned)__shfl((int)(unsigned)(anc >> 32), src);
+        const int jj = __shfl(j, src);
+        if (j >= 0) {
+            anc |= ((unsigned long long)hi << 32) | lo;
+            j = jj;
+        }
+    }
+    if (lane < p.N) {
+        g_anc[lane][0] = anc;
+        g_anc[lane][1] = 0ull;
+        g_anc[lane][2] = 0ull;
+        g_anc[lane][3] = 0ull;
+    }
+}
+
+// The same for up to kMaxNodes nodes, still one wave and no workgroup
+// barrier: lane l owns nodes l, l + 64, ...; sets and jumps of the previous
+// round are read from LDS (double buffered), and a wave-local wait for the
+// LDS writes separates the rounds.
+__device__ void build_ancestor_masks_wave_lds(const AttnParams &p, int b) {
+    constexpr int K = kMaxNodes / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    int jmp[K];
+    #pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int i = lane + k * kWave;
+        jmp[k] = -1;
+        if (i < p.N) {
+            const int pi = p.parent[(size_t)b * p.N + i];
+            jmp[k] = (pi < -1 || pi >= i) ? -1 : pi;
+            #pragma unroll
+            for (int w = 0; w < 4; ++w) g_anc[i][w] = (w == (i >> 6)) ? (1ull << (i & 63)) : 0ull;
+            g_jump[0][i] = jmp[k];
+        }
+    }
     int cur = 0;
-    for (int round = 0; round < 8; ++round) {
+    for (;;) {
+        bool more = false;
+        #pragma unroll
+        for (int k = 0; k < K; ++k) more |= jmp[k] >= 0;
+        if (!__any(more)) break;
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         unsigned long long(*src)[4] = cur == 0 ? g_anc : g_anc_alt;
         unsigned long long(*dst)[4] = cur == 0 ? g_anc_alt : g_anc;
-        int more = 0;
-        for (int i = tid; i < p.N; i += NT) {
-            const int j = g_jump[cur][i];
+        #pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int i = lane + k * kWave;
+            if (i >= p.N) continue;
+            const int j = jmp[k];
             if (j >= 0) {
                 #pragma unroll
                 for (int w = 0; w < 4; ++w) dst[i][w] = src[i][w] | src[j][w];
-                const int jj = g_jump[cur][j];
-                g_jump[cur ^ 1][i] = jj;
-                more |= jj >= 0;
+                jmp[k] = g_jump[cur][j];
             } else {
                 #pragma unroll
                 for (int w = 0; w < 4; ++w) dst[i][w] = src[i][w];
-                g_jump[cur ^ 1][i] = -1;
             }
+            g_jump[cur ^ 1][i] = jmp[k];
         }
         cur ^= 1;
-        if (!__syncthreads_or(more)) break;
     }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     if (cur == 1) {
-        for (int i = tid; i < p.N; i += NT)
-            #pragma unroll
-            for (int w = 0; w < 4; ++w) g_anc[i][w] = g_anc_alt[i][w];
-        __syncthreads();
+        #pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int i = lane + k * kWave;
+            if (i < p.N)
+                #pragma unroll
+                for (int w = 0; w < 4; ++w) g_anc[i][w] = g_anc_alt[i][w];
+        }
     }
 }
 
@@ -785,12 +817,13 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             // sets only when this piece reaches the tree tiles and the workgroup
             // has not built them for this sequence already
             const bool want_anc = first && has_tree && anc_b != b;
-            if ((SMALL && ta < ntp) || want_anc)
-                load_pages_and_parents<NT>(p, b, page_first, npages, SMALL && ta < ntp, want_anc);
+            if (SMALL && ta < ntp) load_pages<NT>(p, b, page_first, npages);
 
             const int T = tb - ta;
             // Load batch i = K tile ta+i and V tile ta+i-1 (those that exist). It is
-            // issued three tile periods before the matrix phase that first needs it.
+            // issued two tile periods before the matrix phase that first needs it
+            // (a third period ahead measured 2 % slower: the extra loads in flight
+            // only lengthen the issue stalls).
             auto batch_loads = [&](int i) {
                 return ((i >= 0 && i < T) ? LPT : 0) + ((i >= 1 && i <= T) ? LPT : 0);
             };
@@ -826,18 +859,24 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             // first tile wait below also covers Q, which was issued earlier.
             ld.set_unit(p, b, g, L, ntp, nodes);
             {
-                int ids[4][LPT];
+                int ids[3][LPT];
                 #pragma unroll
-                for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, ta + i, wave_u, ids[i]);
+                for (int i = 0; i < 3; ++i) ld.fetch_pages(p, b, ta + i, wave_u, ids[i]);
                 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
+                for (int i = 0; i < 3; ++i) {
                     #pragma unroll
                     for (int k = 0; k < LPT; ++k) pk[k] = ids[i][k];
-                    if (i < 3) issue_batch(i);    // pk then holds the ids of batch 3
+                    if (i < 2) issue_batch(i);    // pk then holds the ids of batch 2
                 }
             }
+            // Ancestor sets, while the loads above are in flight, by one wave
+            // (the other waves only read them at the tree tiles, after several
+            // workgroup barriers): in registers up to 64 nodes, else in LDS.
             if (want_anc) {
-                build_ancestor_masks<NT>(p);   // overlaps the loads above
+                if (wave_u == 0) {
+                    if (p.N <= kWave) build_ancestor_masks_wave(p, b);
+                    else build_ancestor_masks_wave_lds(p, b);
+                }
                 anc_b = b;
             }
 
@@ -847,31 +886,28 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             // its start, one at group 0's end). Batch j must have landed, for
             // every wave, before slot 2j: group 0 waits before the barrier that
             // opens its matrix j, group 1 before the one that opens its softmax
-            // j-1. Both groups issue batch j+3 when they start matrix j; the
-            // ring stages it overwrites were last read in slot 2j-1.
+            // j-1. Both groups issue batch j+2 when they start matrix j; the
+            // ring stages it overwrites were last read in slot 2j-3.
             if (grp == 1) {
-                wait_vm_at_most(batch_loads(1) + batch_loads(2));
+                wait_vm_at_most(batch_loads(1));
                 phase_barrier();
             }
-            // slot pair j: barrier, matrix j (issuing batch j+3 along the way);
+            // slot pair j: barrier, matrix j (issuing batch j+2 along the way);
             // barrier, softmax j
             typename Issue::Blocks cur;
             bool have_k = false, have_v = false;
             int stage_k = 0, stage_v = 0;
             // Waits: batch j (group 0, before matrix j) or batch j+1 (group 1,
-            // before softmax j) complete; while the two later batches are full,
-            // that leaves 4 * LPT loads in flight, otherwise wait for all.
+            // before softmax j) complete, leaving this wave's loads of the one
+            // later batch in flight.
             auto open_matrix = [&](int j) {
-                if (grp == 0) {
-                    if (j + 3 <= T) wait_vmcnt<4 * LPT < 63 ? 4 * LPT : 63>();
-                    else wait_vmcnt<0>();
-                }
+                if (grp == 0) wait_vm_at_most(batch_loads(j + 1));
                 phase_barrier();
                 // The matrix phase runs at raised wave priority: when both waves of
                 // a SIMD could issue, its MFMAs and LDS reads go first and the other
                 // group's softmax fills the gaps.
                 __builtin_amdgcn_s_setprio(1);
-                const int i = j + 3;
+                const int i = j + 2;
                 have_k = have_v = false;
                 if (i <= T) {
                     if (SMALL) {
@@ -885,7 +921,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                     }
                 }
             };
-            // Loads of batch j+3 during matrix j: full batches in the steady
+            // Loads of batch j+2 during matrix j: full batches in the steady
             // state, the tail checks which halves exist.
             auto hook_full = [&](int gi) {
                 if (SMALL) return;
@@ -912,21 +948,18 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                 if (!SMALL && have_v) last = cur;
             };
             auto softmax = [&](int j) {
-                if (grp == 1) {
-                    if (j + 4 <= T) wait_vmcnt<4 * LPT < 63 ? 4 * LPT : 63>();
-                    else wait_vmcnt<0>();
-                }
+                if (grp == 1) wait_vm_at_most(batch_loads(j + 2));
                 __builtin_amdgcn_s_setprio(0);
                 phase_barrier();
                 softmax_phase<D>(st, p, ta + j, ntp, L, node, half);
-                fetch(j + 4);          // ids for the batch issued at the next matrix phase
+                fetch(j + 3);          // ids for the batch issued at the next matrix phase
             };
             open_matrix(0);
             matrix_phase<D, false, true>(st, kaddr_of(ta), 0u, hook);
             close_matrix();
             softmax(0);
             int j = 1;
-            for (; j + 3 < T; ++j) {                 // batch j+3 is full
+            for (; j + 2 < T; ++j) {                 // batch j+2 is full
                 open_matrix(j);
                 matrix_phase<D, true, true>(st, kaddr_of(ta + j), vaddr_of(ta + j - 1), hook_full);
                 close_matrix();
