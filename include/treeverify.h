@@ -25,8 +25,10 @@
  *     synchronize. The return value is a status: TV_OK (0) or a negative
  *     TV_ERR_* code. Argument checks are done on the host before anything is
  *     launched; on an error nothing is launched and no output is written.
- *     TV_ERR_HIP reports a launch failure; asynchronous execution errors
- *     surface through the HIP runtime as usual.
+ *     TV_ERR_HIP reports a failure of this call's own launches (each launch
+ *     is checked by its own status, so an error an earlier unrelated HIP call
+ *     left pending is neither reported nor cleared); asynchronous execution
+ *     errors surface through the HIP runtime as usual.
  *   - The library keeps no state between calls apart from a per-device cache
  *     of the compute-unit count. Calls are safe from several host threads as
  *     long as their output buffers do not overlap.

@@ -189,13 +189,12 @@ hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const
                                 int32_t *accept_len, int32_t *accept_idx, int32_t *bonus,
                                 unsigned long long *ws, hipStream_t s) {
     if (B == 0) return hipSuccess;
-    hipLaunchKernelGGL(argmax_segments_kernel, dim3(B * N, segs), dim3(kArgmaxThreads), 0, s,
-                       logits, num_nodes, N, V, segs, seg_len, ws);
-    hipError_t e = hipGetLastError();
+    const hipError_t e = launch_kernel(argmax_segments_kernel, dim3(B * N, segs),
+                                       dim3(kArgmaxThreads), s, logits, num_nodes, N, V, segs,
+                                       seg_len, ws);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(accept_kernel, dim3(B), dim3(kAcceptThreads), 0, s, ws, segs, draft,
-                       parent, num_nodes, N, argmax_out, accept_len, accept_idx, bonus);
-    return hipGetLastError();
+    return launch_kernel(accept_kernel, dim3(B), dim3(kAcceptThreads), s, ws, segs, draft, parent,
+                         num_nodes, N, argmax_out, accept_len, accept_idx, bonus);
 }
 
 }  // namespace tv

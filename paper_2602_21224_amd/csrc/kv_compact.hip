@@ -88,18 +88,16 @@ hipError_t launch_kv_compact(const uint16_t *k_tree, const uint16_t *v_tree, uin
                              int Hkv, int D, int P, int max_pages, int num_pages, hipStream_t s) {
     if (B == 0) return hipSuccess;
     const int p_shift = __builtin_ctz((unsigned)P);
-    hipLaunchKernelGGL(kv_compact_kernel, dim3(N, B), dim3(kCompactThreads), 0, s, k_tree, v_tree,
-                       k_cache, v_cache, page_table, kv_len, accept_idx, accept_len, N, Hkv * D,
-                       P, p_shift, max_pages, num_pages);
-    return hipGetLastError();
+    return launch_kernel(kv_compact_kernel, dim3(N, B), dim3(kCompactThreads), s, k_tree, v_tree,
+                         k_cache, v_cache, page_table, kv_len, accept_idx, accept_len, N, Hkv * D,
+                         P, p_shift, max_pages, num_pages);
 }
 
 hipError_t launch_validate(const int32_t *page_table, const int32_t *kv_len,
                            const int32_t *parent, const int32_t *num_nodes, int B, int N, int P,
                            int max_pages, int num_pages, int32_t *status_word, hipStream_t s) {
-    hipLaunchKernelGGL(validate_kernel, dim3(1), dim3(256), 0, s, page_table, kv_len, parent,
-                       num_nodes, B, N, P, max_pages, num_pages, status_word);
-    return hipGetLastError();
+    return launch_kernel(validate_kernel, dim3(1), dim3(256), s, page_table, kv_len, parent,
+                         num_nodes, B, N, P, max_pages, num_pages, status_word);
 }
 
 }  // namespace tv

@@ -1094,19 +1094,16 @@ __global__ __launch_bounds__(256) void tree_attention_merge_kernel(AttnParams p,
 
 template <int D, int NW>
 hipError_t launch_dn(const AttnParams &p, hipStream_t s) {
-    if (p.small_pages)
-        hipLaunchKernelGGL((tree_attention_kernel<D, NW, true>), dim3(p.num_wg), dim3(NW * kWave), 0, s, p);
-    else
-        hipLaunchKernelGGL((tree_attention_kernel<D, NW, false>), dim3(p.num_wg), dim3(NW * kWave), 0, s, p);
-    hipError_t e = hipGetLastError();
+    hipError_t e = p.small_pages
+        ? launch_kernel(tree_attention_kernel<D, NW, true>, dim3(p.num_wg), dim3(NW * kWave), s, p)
+        : launch_kernel(tree_attention_kernel<D, NW, false>, dim3(p.num_wg), dim3(NW * kWave), s, p);
     if (e != hipSuccess) return e;
     if (p.num_wg > 1) {
         constexpr int kRowsPerWg = 256 / (D / 8);
         const int chunks = (p.rows_per_block + kRowsPerWg - 1) / kRowsPerWg;
         const int stride = (p.num_wg + kNumXcd - 1) / kNumXcd * kNumXcd;
-        hipLaunchKernelGGL((tree_attention_merge_kernel<D>), dim3(stride * chunks), dim3(256), 0, s, p,
-                           stride);
-        e = hipGetLastError();
+        e = launch_kernel(tree_attention_merge_kernel<D>, dim3(stride * chunks), dim3(256), s, p,
+                          stride);
     }
     return e;
 }

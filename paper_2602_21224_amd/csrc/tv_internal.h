@@ -4,6 +4,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <tuple>
+#include <type_traits>
+#include <utility>
+
 namespace tv {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -50,6 +54,22 @@ __device__ __forceinline__ int xcd_contiguous_id(int hw_id, int n) {
     const int local = hw_id / kNumXcd;
     const int base = xcd * (n / kNumXcd) + min(xcd, n % kNumXcd);
     return base + local;
+}
+
+// Launch a kernel and return the runtime's status for this launch alone
+// (hipGetLastError after hipLaunchKernelGGL would also report an error left
+// behind by an unrelated earlier call of the caller's).
+template <typename... KArgs, typename... Args>
+inline hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s,
+                                Args &&...args) {
+    static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel argument count");
+    std::tuple<std::decay_t<KArgs>...> held(std::forward<Args>(args)...);
+    return std::apply(
+        [&](auto &...a) {
+            void *ptrs[] = {static_cast<void *>(&a)...};
+            return hipLaunchKernel(reinterpret_cast<const void *>(kernel), grid, block, ptrs, 0, s);
+        },
+        held);
 }
 
 // Host-side launchers (defined next to their kernels).

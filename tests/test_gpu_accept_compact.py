@@ -139,3 +139,53 @@ def test_validate_inputs():
     st = T.tv_validate_inputs(U.dev(bad_pt), U.dev(w.kv_len), U.dev(bad_parent), P=w.P,
                               num_pages=w.num_pages)
     assert int(st.item()) == (1 | 8)
+
+
+def test_unrelated_runtime_error_is_not_reported(oracle_mod):
+    """An error left in the HIP runtime by an earlier, unrelated call of the
+    caller's neither turns correct calls into failures nor is consumed by them:
+    every launch is checked by its own status."""
+    import ctypes
+    T = U.require_gpu()
+    hip = None
+    with open("/proc/self/maps") as fh:
+        for line in fh:
+            if "libamdhip64" in line:
+                hip = ctypes.CDLL(line.split()[-1])
+                break
+    assert hip is not None
+    w = W.preset("tiny")
+    d = U.upload(w)
+    logits, draft, parent = U.dev(w.logits), U.dev(w.draft), U.dev(w.parent)
+    out = torch.empty((w.B, w.N, w.Hq, w.D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((w.B, w.N, w.Hq), dtype=torch.float32, device="cuda")
+    amax = torch.empty((w.B, w.N), dtype=torch.int32, device="cuda")
+    alen = torch.empty((w.B,), dtype=torch.int32, device="cuda")
+    aidx = torch.empty((w.B, w.N), dtype=torch.int32, device="cuda")
+    bonus = torch.empty((w.B,), dtype=torch.int32, device="cuda")
+    ws_a = torch.empty(T.attention_workspace_size(w.B, w.N, w.Hq, w.Hkv, w.D), dtype=torch.uint8,
+                       device="cuda")
+    ws_m = torch.empty(T.argmax_workspace_size(w.B, w.N, w.V), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    print("case stale error: hipSetDevice(99999) before the calls", flush=True)
+    assert hip.hipSetDevice(ctypes.c_int(99999)) != 0      # host-side check, nothing launched
+    try:
+        T.tree_argmax_accept(logits, draft, parent, argmax_out=amax, accept_len=alen,
+                             accept_idx=aidx, bonus_token=bonus, workspace=ws_m)
+        T.tree_verify_attention(d["q"], d["k_tree"], d["v_tree"], d["k_cache"], d["v_cache"],
+                                d["page_table"], d["kv_len"], d["parent"], max_kv_len=w.max_kv_len,
+                                out=out, lse=lse, workspace=ws_a)
+        assert hip.hipPeekAtLastError() != 0               # still the caller's to collect
+    finally:
+        hip.hipGetLastError()
+    torch.cuda.synchronize()
+    ra = oracle_mod.argmax(w.logits)
+    np.testing.assert_array_equal(amax.cpu().numpy(), ra)
+    rl, ri, rb = oracle_mod.accept(w.draft, w.parent, ra)
+    np.testing.assert_array_equal(alen.cpu().numpy(), rl)
+    np.testing.assert_array_equal(aidx.cpu().numpy(), ri)
+    np.testing.assert_array_equal(bonus.cpu().numpy(), rb)
+    want, wlse = oracle_mod.tree_attention(w.q, w.k_tree, w.v_tree, w.k_cache, w.v_cache,
+                                           w.page_table, w.kv_len, w.parent)
+    U.assert_attention_close(U.bf16_to_f64(out), want, lse.cpu().numpy().astype(np.float64), wlse,
+                             "stale-error")
