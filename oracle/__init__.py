@@ -4,9 +4,11 @@ Only `tests/`, `__graft_entry__.smoke()` and the benchmark's `cpu_baseline`
 leg may import this package. The GPU library never links, loads or calls it,
 and it shares no code with the GPU library.
 
-The arithmetic lives in `oracle.c` (plain C, fp64, OpenMP across independent
-items); this module only compiles it with gcc and marshals numpy arrays.
-Each wrapper cites the passage of the paper the C function follows.
+The verification arithmetic lives in `oracle.c` (plain C, fp64, OpenMP across
+independent items); this module only compiles it with gcc and marshals numpy
+arrays. Each wrapper cites the passage of the paper the C function follows.
+The draft-tree builder (Alg. 1 with budget pruning) is `tree_build.py`, plain
+numpy.
 """
 from __future__ import annotations
 
@@ -197,3 +199,6 @@ def kv_compact(k_tree, v_tree, k_cache, v_cache, page_table, kv_len, accept_idx,
     if rc != 0:
         raise ValueError("oracle_kv_compact: destination outside the page table or pool")
     return kc, vc
+
+
+from .tree_build import tree_build  # noqa: E402  (Alg. 1 + budget pruning, numpy)
