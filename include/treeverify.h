@@ -73,7 +73,7 @@ extern "C" {
 #define TV_API
 #endif
 
-#define TV_ABI_VERSION 2
+#define TV_ABI_VERSION 3
 
 enum tv_status {
     TV_OK = 0,
@@ -223,6 +223,60 @@ TV_API int tv_validate_inputs(const int32_t *page_table, const int32_t *kv_len,
                               const int32_t *parent, const int32_t *num_nodes, int B, int N,
                               int P, int max_pages, int num_pages, int32_t *status_word,
                               hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * tree_build  (draft-tree construction by token-info sampling, Alg. 1 of
+ *              §5.2, followed by the verification-budget pruning of §5.2;
+ *              the hot-token table of §6.1)
+ *
+ * For each sequence b: the root is root_token[b] (the last verified token,
+ * probability and joint probability 1) and forms the first frontier. At step
+ * i = 0 .. S-1, every frontier node (in frontier order) takes the k most
+ * probable tokens of softmax(logits[b][i] + r) as its children, in rank order,
+ * where r is the node token's row of the token-info table (§5.1: the collapsed
+ * token-info embedding adds to the logits); a child's joint probability is its
+ * parent's times its own. The next frontier is the k children of the step with
+ * the largest joint probabilities, largest first. After the last step the
+ * `budget` nodes of largest joint probability are kept, in creation order
+ * (root first; a node's parent always precedes it and is always kept).
+ *
+ * Hot tokens (§6.1): token-info exists for the H hot tokens only.
+ * hot_vocab[c] is the vocabulary id of hot token c (distinct ids) and
+ * hot_index[v] = c for v = hot_vocab[c], -1 for every other v. token_info is
+ * [H, H] bf16: entry (row, col) is added to the logit of hot token col when
+ * the expanded node's token is hot token row. A node whose token is not hot,
+ * and every non-hot candidate, get nothing added. With H = 0 the three hot
+ * arrays may be NULL.
+ *
+ * Arithmetic: candidates are ranked by the fp32 sum logit + entry (ties to
+ * the lower vocabulary id); probabilities and joint probabilities are fp64
+ * (ties in joint probability go to the node created first: step, frontier
+ * rank, child rank).
+ *
+ *   logits       [B, S, V]   fp32, finite (the draft model's logits per step)
+ *   root_token   [B]         int32 in [0, V)
+ *   token_info   [H, H]      bf16; hot_vocab [H], hot_index [V] int32
+ *   parent       [B, budget] int32 out: parent slot, -1 for the root and padding
+ *   token        [B, budget] int32 out: the node's token, -1 for padding
+ *   joint        [B, budget] fp32 out: joint probability, 0 for padding
+ *   num_nodes    [B]         int32 out: min(budget, 1 + k + (S-1) k^2); slots
+ *                            from num_nodes[b] on are padding. (parent, token,
+ *                            num_nodes) are the tree inputs of
+ *                            tree_verify_attention / tree_argmax_accept.
+ *   workspace    >= tv_tree_build_workspace_size(...) bytes of device memory,
+ *                8-byte aligned; contents on entry do not matter; clobbered.
+ *
+ * Supported: 0 <= B <= 65535, 1 <= S <= 16, 1 <= k <= 16, k <= V,
+ * 0 <= H <= V, 1 <= budget <= 256. Contract (not checked): consistent hot
+ * maps, root tokens in range. Out-of-range hot ids are skipped; results for
+ * inputs that break the contract are unspecified.
+ * ------------------------------------------------------------------------ */
+TV_API size_t tv_tree_build_workspace_size(int B, int S, int V, int H, int k);
+TV_API int tree_build(const float *logits, const int32_t *root_token, const uint16_t *token_info,
+                      const int32_t *hot_vocab, const int32_t *hot_index, int B, int S, int V,
+                      int H, int k, int budget, int32_t *parent, int32_t *token, float *joint,
+                      int32_t *num_nodes, void *workspace, size_t workspace_bytes,
+                      hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -55,8 +55,8 @@ def build_tree_one(logits: np.ndarray, root: int, table: np.ndarray, hot: np.nda
                    margins: list | None = None):
     """Alg. 1 for one sequence without pruning.
 
-    logits [S, V] float32, root token id, table [H, H] float32 (bf16 values),
-    hot [H] vocab ids. Returns parallel lists (token, parent, prob, joint) in
+    logits [S, V] float32, root token id, table [H, H] float32 (bf16 values)
+    or uint16 (bf16 bit patterns, converted one row at a time), hot [H] vocab ids. Returns parallel lists (token, parent, prob, joint) in
     creation order. When `margins` is a list, the relative gap between the
     last frontier node kept and the first one dropped is appended per step.
     """
@@ -72,7 +72,10 @@ def build_tree_one(logits: np.ndarray, root: int, table: np.ndarray, hot: np.nda
             x = l_i.copy()
             h = hot_index[token[f]]
             if h >= 0:
-                x[hot] = (l_i[hot] + table[h]).astype(np.float32)
+                row = table[h]
+                if row.dtype == np.uint16:
+                    row = bf16_bits_to_f32(row)
+                x[hot] = (l_i[hot] + row).astype(np.float32)
             x64 = x.astype(np.float64)
             m = x64.max()
             s = np.exp(x64 - m).sum()
@@ -112,11 +115,13 @@ def tree_build(logits, root, table_bits, hot, k: int, budget: int, margins: list
 
     logits [B, S, V] float32; root [B] int32; table_bits [H, H] uint16 (bf16);
     hot [H] int32 distinct vocab ids. Returns parent [B, budget] int32, token
-    [B, budget] int32, joint [B, budget] float64 and num_nodes [B] int32.
+    [B, budget] int32, joint [B, budget] float64 and num_nodes [B] int32. With a
+    `margins` list, the relative gap at every frontier choice and at the
+    pruning cut is appended (how close the decision was to a tie).
     """
     logits = np.asarray(logits, dtype=np.float32)
     B = logits.shape[0]
-    table = bf16_bits_to_f32(table_bits)
+    table = np.asarray(table_bits, dtype=np.uint16)
     hot = np.asarray(hot, dtype=np.int64)
     par = np.full((B, budget), -1, dtype=np.int32)
     tok = np.full((B, budget), -1, dtype=np.int32)
@@ -124,5 +129,8 @@ def tree_build(logits, root, table_bits, hot, k: int, budget: int, margins: list
     nn = np.zeros(B, dtype=np.int32)
     for b in range(B):
         t, p, _, j = build_tree_one(logits[b], int(root[b]), table, hot, k, margins)
+        if margins is not None and len(j) > budget:
+            js = sorted(j, reverse=True)
+            margins.append((js[budget - 1] - js[budget]) / js[budget - 1])
         par[b], tok[b], jnt[b], nn[b] = prune(t, p, j, budget)
     return par, tok, jnt, nn

@@ -50,6 +50,10 @@ def load():
     lib.kv_compact_accepted.restype = i
     lib.tv_validate_inputs.argtypes = [p] * 4 + [i] * 5 + [p, p]
     lib.tv_validate_inputs.restype = i
+    lib.tv_tree_build_workspace_size.argtypes = [i] * 5
+    lib.tv_tree_build_workspace_size.restype = sz
+    lib.tree_build.argtypes = [p] * 5 + [i] * 6 + [p] * 5 + [sz, p]
+    lib.tree_build.restype = i
     _lib = lib
     return lib
 
@@ -207,3 +211,48 @@ def tv_validate_inputs(page_table, kv_len, parent, *, P: int, num_pages: int, nu
                                    max_pages, num_pages, _ptr(word), _stream(stream))
     _check(st, "tv_validate_inputs")
     return word
+
+
+def tree_build_workspace_size(B, S, V, H, k) -> int:
+    return int(load().tv_tree_build_workspace_size(B, S, V, H, k))
+
+
+def tree_build(logits, root_token, token_info, hot_vocab, hot_index, *, k: int, budget: int,
+               parent=None, token=None, joint=None, num_nodes=None, workspace=None, stream=None):
+    """Draft tree by token-info sampling (Alg. 1) pruned to `budget` nodes (§5.2).
+
+    logits [B, S, V] fp32, root_token [B] int32, token_info [H, H] bf16 (or
+    None with H = 0), hot_vocab [H] and hot_index [V] int32. Returns (parent,
+    token, joint, num_nodes): [B, budget] int32, int32, fp32 and [B] int32.
+    """
+    B, S, V = logits.shape
+    _want(logits, "logits", (torch.float32,))
+    _want(root_token, "root_token", (torch.int32,), (B,))
+    H = 0 if token_info is None else token_info.shape[0]
+    if H > 0:
+        _want(token_info, "token_info", _BF16, (H, H))
+        _want(hot_vocab, "hot_vocab", (torch.int32,), (H,))
+        _want(hot_index, "hot_index", (torch.int32,), (V,))
+    dev = logits.device
+    mk = lambda shape, dt: torch.empty(shape, dtype=dt, device=dev)
+    parent = mk((B, budget), torch.int32) if parent is None else parent
+    token = mk((B, budget), torch.int32) if token is None else token
+    joint = mk((B, budget), torch.float32) if joint is None else joint
+    num_nodes = mk((B,), torch.int32) if num_nodes is None else num_nodes
+    _want(parent, "parent", (torch.int32,), (B, budget))
+    _want(token, "token", (torch.int32,), (B, budget))
+    _want(joint, "joint", (torch.float32,), (B, budget))
+    _want(num_nodes, "num_nodes", (torch.int32,), (B,))
+    need = tree_build_workspace_size(B, S, V, H, k)
+    if need == 0:
+        raise TreeVerifyError(f"tree_build: unsupported shape B={B} S={S} V={V} H={H} k={k}")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    st = load().tree_build(
+        _ptr(logits), _ptr(root_token), _ptr(token_info if H > 0 else None),
+        _ptr(hot_vocab if H > 0 else None), _ptr(hot_index if H > 0 else None), B, S, V, H, k,
+        budget, _ptr(parent), _ptr(token), _ptr(joint), _ptr(num_nodes), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "tree_build")
+    return parent, token, joint, num_nodes
+

@@ -25,19 +25,6 @@ namespace {
 constexpr int kArgmaxThreads = 256;
 constexpr int kAcceptThreads = 256;
 
-// Order-preserving key of a float: larger value -> larger key; NaN largest;
-// -0 and +0 equal.
-__device__ __forceinline__ unsigned int value_key(float x) {
-    unsigned int u = __float_as_uint(x);
-    if (x != x) return 0xFFFFFFFFu;
-    if (x == 0.f) u = 0u;
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ unsigned long long pack(unsigned int key, unsigned int idx) {
-    return ((unsigned long long)key << 32) | (unsigned long long)(0xFFFFFFFFu - idx);
-}
-
 __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
     return a > b ? a : b;
 }
@@ -79,7 +66,7 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_segments_kernel(
     const int head = (int)(((16 - (addr & 15)) & 15) / 4);
     const int vh = min(v1, v0 + head);
     for (int v = v0 + tid; v < vh; v += kArgmaxThreads)
-        best = umax64(best, pack(value_key(x[v]), (unsigned int)v));
+        best = umax64(best, pack_key(order_key(x[v]), (unsigned int)v));
     const int nvec = (v1 - vh) / 4;
     const f32x4 *xv = reinterpret_cast<const f32x4 *>(x + vh);
     constexpr int U = 4;
@@ -92,17 +79,17 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_segments_kernel(
         for (int u = 0; u < U; ++u) {
             const unsigned int base = (unsigned int)(vh + 4 * (i + u * kArgmaxThreads));
             #pragma unroll
-            for (int k = 0; k < 4; ++k) best = umax64(best, pack(value_key(r[u][k]), base + k));
+            for (int k = 0; k < 4; ++k) best = umax64(best, pack_key(order_key(r[u][k]), base + k));
         }
     }
     for (; i < nvec; i += kArgmaxThreads) {
         const f32x4 r = __builtin_nontemporal_load(xv + i);
         const unsigned int base = (unsigned int)(vh + 4 * i);
         #pragma unroll
-        for (int k = 0; k < 4; ++k) best = umax64(best, pack(value_key(r[k]), base + k));
+        for (int k = 0; k < 4; ++k) best = umax64(best, pack_key(order_key(r[k]), base + k));
     }
     for (int v = vh + 4 * nvec + tid; v < v1; v += kArgmaxThreads)
-        best = umax64(best, pack(value_key(x[v]), (unsigned int)v));
+        best = umax64(best, pack_key(order_key(x[v]), (unsigned int)v));
 
     best = wave_max64(best);
     __shared__ unsigned long long part[kArgmaxThreads / kWave];

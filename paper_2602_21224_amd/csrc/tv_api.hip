@@ -259,4 +259,38 @@ int tv_validate_inputs(const int32_t *page_table, const int32_t *kv_len, const i
     return e == hipSuccess ? TV_OK : TV_ERR_HIP;
 }
 
+static bool tree_build_shape_ok(int B, int S, int V, int H, int k) {
+    return B >= 0 && B <= 65535 && S >= 1 && S <= tv::kTbMaxSteps && V >= 1 && H >= 0 &&
+           H <= V && k >= 1 && k <= tv::kTbMaxK && k <= V;
+}
+
+size_t tv_tree_build_workspace_size(int B, int S, int V, int H, int k) {
+    if (!tree_build_shape_ok(B, S, V, H, k)) return 0;
+    const tv::TreeBuildPlan pl = tv::tree_build_plan(B, S, V, H, k);
+    const size_t nn = (size_t)B * pl.max_nodes;
+    return round_up(pl.rows_bytes, 256) + round_up(pl.parts_bytes, 256) +
+           2 * round_up(nn * sizeof(int32_t), 256) + round_up(nn * sizeof(double), 256) +
+           round_up(pl.frontier_bytes, 256) + 256;
+}
+
+int tree_build(const float *logits, const int32_t *root_token, const uint16_t *token_info,
+               const int32_t *hot_vocab, const int32_t *hot_index, int B, int S, int V, int H,
+               int k, int budget, int32_t *parent, int32_t *token, float *joint,
+               int32_t *num_nodes, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!tree_build_shape_ok(B, S, V, H, k) || budget < 1 || budget > tv::kMaxNodes)
+        return TV_ERR_SHAPE;
+    if (B == 0) return TV_OK;
+    if (!logits || !root_token || !parent || !token || !joint || !num_nodes || !workspace ||
+        (H > 0 && (!token_info || !hot_vocab || !hot_index)))
+        return TV_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(logits) & 3u) || (reinterpret_cast<uintptr_t>(workspace) & 7u))
+        return TV_ERR_ALIGN;
+    if (workspace_bytes < tv_tree_build_workspace_size(B, S, V, H, k)) return TV_ERR_WORKSPACE;
+    if (!device_ok()) return TV_ERR_DEVICE;
+    const hipError_t e = tv::launch_tree_build(logits, root_token, token_info, hot_vocab,
+                                               hot_index, B, S, V, H, k, budget, parent, token,
+                                               joint, num_nodes, workspace, stream);
+    return e == hipSuccess ? TV_OK : TV_ERR_HIP;
+}
+
 }  // extern "C"

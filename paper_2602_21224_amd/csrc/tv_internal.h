@@ -26,6 +26,32 @@ constexpr int kKeyTile = 64;         // keys per attention tile (two 32-key MFMA
 constexpr int kRowsPerWave = 32;     // query rows per wave (MFMA N dimension)
 constexpr int kMaxNodes = 256;
 constexpr int kMaxBatchAttn = 1024;
+constexpr int kTbMaxK = 16;          // tree builder: largest branch number
+constexpr int kTbMaxSteps = 16;      // tree builder: most speculative steps
+
+// Order-preserving key of a float: larger value -> larger key; NaN largest;
+// -0 and +0 equal.
+__device__ __forceinline__ unsigned int order_key(float x) {
+    unsigned int u = __float_as_uint(x);
+    if (x != x) return 0xFFFFFFFFu;
+    if (x == 0.f) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// (value key, index) packed so that a plain unsigned maximum picks the larger
+// value and, among equal values, the lower index.
+__device__ __forceinline__ unsigned long long pack_key(unsigned int key, unsigned int idx) {
+    return ((unsigned long long)key << 32) | (unsigned long long)(0xFFFFFFFFu - idx);
+}
+
+// Launch geometry and workspace layout of the tree builder.
+struct TreeBuildPlan {
+    int segs, seg_len;         // vocabulary segments per (sequence, step) row
+    int chunks, chunk_len;     // hot-column chunks per frontier node (0 without hot tokens)
+    int max_nodes;             // nodes of the unpruned tree: 1 + k + (S - 1) k^2
+    size_t rows_bytes, parts_bytes, nodes_bytes, frontier_bytes;
+};
+TreeBuildPlan tree_build_plan(int B, int S, int V, int H, int k);
 
 // Launch parameters of the tree-attention kernels (all sizes in elements).
 struct AttnParams {
@@ -73,6 +99,11 @@ inline hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block,
 }
 
 // Host-side launchers (defined next to their kernels).
+hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
+                             const uint16_t *table, const int32_t *hot_vocab,
+                             const int32_t *hot_index, int B, int S, int V, int H, int k,
+                             int budget, int32_t *parent, int32_t *token, float *joint,
+                             int32_t *num_nodes, void *workspace, hipStream_t s);
 hipError_t launch_tree_attention(const AttnParams &p, int head_dim, int waves, hipStream_t s);
 hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const int32_t *parent,
                                 const int32_t *num_nodes, int B, int N, int V, int segs,

@@ -395,3 +395,76 @@ PRESET_DOC = {
                           "sequence a 24-48-node tree plus a 0-16-node re-sampled tree "
                           "(second root), padded to 64, vocab 128256, seed 5",
 }
+
+
+# ---------------------------------------------------------------------------
+# Inputs of the draft-tree builder (token-info sampling, Alg. 1 of §5.2, with
+# the hot-token table of §6.1): per-step draft logits, a root token per
+# sequence, the hot-token list and the bf16 token-info table over it.
+@dataclass
+class TreeBuildInputs:
+    name: str
+    B: int
+    S: int          # speculative steps (rows of draft logits per sequence)
+    V: int
+    H: int          # hot tokens (0: no token information)
+    k: int          # branch number
+    budget: int     # verification token budget
+    logits: np.ndarray     # [B, S, V] float32
+    root: np.ndarray       # [B] int32
+    table: np.ndarray      # [H, H] uint16 (bf16 bits)
+    hot_vocab: np.ndarray  # [H] int32, distinct vocabulary ids
+    hot_index: np.ndarray  # [V] int32, -1 for tokens without token-info
+
+
+def make_tree_build_inputs(name: str, seed: int, *, B: int, S: int, V: int, H: int, k: int,
+                           budget: int, logit_scale: float = 2.5,
+                           info_scale: float = 1.0) -> TreeBuildInputs:
+    """Seeded synthetic builder inputs. Draft logits are N(0, logit_scale^2)
+    (peaked enough that a few tokens carry most of the mass); the hot set is a
+    seeded random subset of the vocabulary (a stand-in for the corpus
+    frequency ranking of §6.1); table entries are uniform with standard
+    deviation info_scale, cut to bf16; roots are hot tokens with probability
+    0.75."""
+    ss = np.random.SeedSequence(seed)
+    r_log, r_hot, r_tab, r_root = (np.random.default_rng(s) for s in ss.spawn(4))
+    logits = np.empty((B, S, V), dtype=np.float32)
+    for b in range(B):
+        logits[b] = r_log.standard_normal((S, V), dtype=np.float32) * np.float32(logit_scale)
+    hot_vocab = r_hot.permutation(V)[:H].astype(np.int32)
+    hot_index = np.full(V, -1, dtype=np.int32)
+    hot_index[hot_vocab] = np.arange(H, dtype=np.int32)
+    table = np.empty((H, H), dtype=np.uint16)
+    step = max(1, (1 << 24) // max(H, 1))
+    for r0 in range(0, H, step):
+        r1 = min(H, r0 + step)
+        x = r_tab.random((r1 - r0, H), dtype=np.float32)
+        x = (x - np.float32(0.5)) * np.float32(2.0 * 3.0 ** 0.5 * info_scale)
+        table[r0:r1] = (x.view(np.uint32) >> 16).astype(np.uint16)     # bf16 by truncation
+    root = r_root.integers(0, V, B).astype(np.int32)
+    if H > 0:
+        use_hot = r_root.random(B) < 0.75
+        root[use_hot] = hot_vocab[r_root.integers(0, H, int(use_hot.sum()))]
+    return TreeBuildInputs(name, B, S, V, H, k, budget, logits, root, table, hot_vocab,
+                           hot_index)
+
+
+TREE_BUILD_PRESETS = {
+    # name: (seed, B, S, V, H, k, budget)
+    "tb_tiny": (40, 2, 3, 300, 60, 3, 16),
+    "tb_llama2_bs16": (41, 16, 7, 32000, 32000, 8, 64),
+    "tb_llama8b_bs16": (42, 16, 7, 128256, 32768, 8, 64),
+}
+
+TREE_BUILD_DOC = {
+    "tb_tiny": "batch 2, 3 steps, vocab 300 with 60 hot tokens, k 3, budget 16",
+    "tb_llama2_bs16": "batch 16, 7 steps, vocab 32000 (all hot: below the 40K threshold of "
+                      "§6.1), k 8, budget 64",
+    "tb_llama8b_bs16": "batch 16, 7 steps, vocab 128256 with the 32768 hot tokens of §6.1, "
+                       "k 8, budget 64",
+}
+
+
+def tree_build_preset(name: str) -> TreeBuildInputs:
+    seed, B, S, V, H, k, budget = TREE_BUILD_PRESETS[name]
+    return make_tree_build_inputs(name, seed, B=B, S=S, V=V, H=H, k=k, budget=budget)

@@ -47,7 +47,7 @@ def test_only_declared_symbols_are_exported():
 
 
 def test_status_strings(lib):
-    assert lib.tv_abi_version() == 2
+    assert lib.tv_abi_version() == 3
     for code in range(0, -7, -1):
         assert lib.tv_status_string(code)
     assert lib.tv_status_string(-99) == b"unknown status"
@@ -113,3 +113,27 @@ def test_accept_and_compact_argument_checks(lib):
     assert cmp_(P=3) == -2
     assert cmp_(Hkv=1, D=6) == -2
     assert cmp_(kt=ctypes.c_void_p(0x10004)) == -3
+
+
+def tb(lib, **kw):
+    a = dict(logits=FAKE, root=FAKE, table=FAKE, hot_vocab=FAKE, hot_index=FAKE, B=2, S=4, V=1000,
+             H=100, k=4, budget=32, parent=FAKE, token=FAKE, joint=FAKE, num_nodes=FAKE, ws=FAKE,
+             ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.tree_build(*a.values(), STREAM)
+
+
+def test_tree_build_argument_checks(lib):
+    assert tb(lib, B=0) == 0
+    assert tb(lib, logits=NULL) == -1 and tb(lib, num_nodes=NULL) == -1
+    assert tb(lib, table=NULL) == -1                      # hot tokens need their table
+    assert tb(lib, S=0) == -2 and tb(lib, S=17) == -2
+    assert tb(lib, k=0) == -2 and tb(lib, k=17) == -2 and tb(lib, k=5, V=4, H=0) == -2
+    assert tb(lib, H=1001) == -2 and tb(lib, H=-1) == -2
+    assert tb(lib, budget=0) == -2 and tb(lib, budget=257) == -2
+    assert tb(lib, logits=ctypes.c_void_p(0x10002)) == -3
+    assert tb(lib, ws=ctypes.c_void_p(0x10004)) == -3
+    need = lib.tv_tree_build_workspace_size(2, 4, 1000, 100, 4)
+    assert need > 0 and tb(lib, ws_bytes=need - 1) == -4
+    assert lib.tv_tree_build_workspace_size(2, 0, 1000, 100, 4) == 0
+
