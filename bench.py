@@ -141,6 +141,7 @@ CALL_KERNELS = {
     "tree_verify_attention": ("tree_attention_kernel", "tree_attention_merge_kernel"),
     "tree_argmax_accept": ("argmax_segments_kernel", "accept_kernel"),
     "kv_compact_accepted": ("kv_compact_kernel",),
+    "tree_build": ("tb_rows_kernel", "tb_expand_kernel", "tb_select_kernel", "tb_prune_kernel"),
 }
 
 
@@ -178,11 +179,13 @@ def write_traffic(workload: str, fetch_dir: str, write_dir: str, copy_fetch_dir:
     for call, kernels in CALL_KERNELS.items():
         per = {}
         total = 0.0
+        calls = len(fv.get(kernels[0], []))          # the first kernel runs once per call
         for k in kernels:
-            if k not in fv or k not in wv:
+            if k not in fv or k not in wv or calls == 0:
                 continue
-            fb = np.mean(fv[k]) * 1024.0 * fetch_scale
-            wb = np.mean(wv[k]) * 1024.0 * write_scale
+            # bytes per call: a kernel may run several times per call
+            fb = np.sum(fv[k]) / calls * 1024.0 * fetch_scale
+            wb = np.sum(wv[k]) / calls * 1024.0 * write_scale
             per[k] = {"fetch_bytes": int(round(fb)), "write_bytes": int(round(wb)),
                       "dispatches": len(fv[k])}
             total += fb + wb
@@ -228,6 +231,101 @@ def cpu_baseline(w, sample_b: int, min_seconds: float = 10.0):
                       f"(fp64 C, OpenMP), {dt:.2f} s"}
 
 
+def tree_build_bytes(x) -> int:
+    """Bytes the tree builder must move per call: every step's logits once,
+    the hot map once, one table row per expanded node, the outputs."""
+    expanded = x.B * (1 + (x.S - 1) * x.k)           # nodes whose children are drawn
+    return (x.B * x.S * x.V * 4 + (x.V * 4 + x.H * 4 if x.H else 0) + expanded * x.H * 2
+            + x.B * x.budget * 12 + x.B * 8)
+
+
+def run_tree_build(args, T, torch):
+    """The draft-tree builder (token-info sampling, Alg. 1, and budget
+    pruning) on one batch per step; value = draft trees per second."""
+    from paper_2602_21224_amd import workloads as W
+    x = W.tree_build_preset(args.workload)
+    dev = torch.device("cuda:0")
+    print(f"# workload {args.workload}: B={x.B} S={x.S} V={x.V} H={x.H} k={x.k} "
+          f"budget={x.budget}", file=sys.stderr, flush=True)
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    table = up(x.table.view(np.int16)).view(torch.bfloat16) if x.H else None
+    hot_vocab = up(x.hot_vocab) if x.H else None
+    hot_index = up(x.hot_index) if x.H else None
+    copies = [dict(logits=up(x.logits), root=up(x.root))]
+    copies += [{k: v.clone() for k, v in copies[0].items()} for _ in range(args.copies - 1)]
+    ws = torch.empty(T.tree_build_workspace_size(x.B, x.S, x.V, x.H, x.k), dtype=torch.uint8,
+                     device=dev)
+    outs = [dict(parent=torch.empty((x.B, x.budget), dtype=torch.int32, device=dev),
+                 token=torch.empty((x.B, x.budget), dtype=torch.int32, device=dev),
+                 joint=torch.empty((x.B, x.budget), dtype=torch.float32, device=dev),
+                 nn=torch.empty((x.B,), dtype=torch.int32, device=dev)) for _ in copies]
+    stream = torch.cuda.current_stream()
+    tev = TimingEvents()
+
+    def step(i, ev=None):
+        c, o = copies[i % len(copies)], outs[i % len(copies)]
+        if ev: tev.record(ev[0], stream)
+        T.tree_build(c["logits"], c["root"], table, hot_vocab, hot_index, k=x.k, budget=x.budget,
+                     parent=o["parent"], token=o["token"], joint=o["joint"], num_nodes=o["nn"],
+                     workspace=ws)
+        if ev: tev.record(ev[1], stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ev_every = max(1, min(4, args.steps // 8))
+    evs = [[tev.create() for _ in range(2)] if i % ev_every == 0 else None
+           for i in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    sampled = [e for e in evs if e is not None]
+    t_call = np.array([tev.seconds(e[0], e[1]) for e in sampled])
+    for e in sampled:
+        for q in e:
+            tev.destroy(q)
+    nbytes = tree_build_bytes(x)
+    ach = nbytes / t_call.mean() / 1e9
+    cpu = None
+    if args.cpu_sample != 0:
+        import oracle
+        nb = x.B if args.cpu_sample < 0 else min(args.cpu_sample, x.B)
+        reps, c0 = 0, time.perf_counter()
+        while True:
+            oracle.tree_build(x.logits[:nb], x.root[:nb], x.table, x.hot_vocab, x.k, x.budget)
+            reps += 1
+            dt = time.perf_counter() - c0
+            if dt >= 10.0 or reps >= 50:
+                break
+        cpu = {"value": round(reps * nb / dt, 2), "unit": "draft trees/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"{nb} of {x.B} sequences of the same workload, {reps} passes "
+                         f"(numpy, one thread), {dt:.2f} s"}
+    line = {
+        "metric": "draft trees/sec (token-info sampling + budget pruning), 1 GPU",
+        "value": round(x.B / (wall / args.steps), 1), "unit": "draft trees/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32+f64", "data": "synthetic",
+        "config": {"workload": args.workload, "batch": x.B, "steps": x.S, "vocab": x.V,
+                   "hot_tokens": x.H, "branch": x.k, "budget": x.budget,
+                   "input_copies_rotated": len(copies)},
+        "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                     "traffic": load_traffic("tree_build", args.workload), "kernel": "tree_build",
+                     "avg_us": round(t_call.mean() * 1e6, 2), "algorithmic_bytes": int(nbytes),
+                     "launches_per_call": 2 * x.S + 2},
+        "call_us_p50": round(float(np.median(t_call)) * 1e6, 2),
+        "timed_steps_with_events": len(sampled),
+        "cpu_baseline": cpu,
+        "source_digest": source_digest(),
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -271,6 +369,9 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
         return
     T.load()
+    if args.workload in W.TREE_BUILD_PRESETS:
+        run_tree_build(args, T, torch)
+        return
     w = W.preset(args.workload)
     print(f"# workload {args.workload}: B={w.B} N={w.N} Hq={w.Hq} Hkv={w.Hkv} D={w.D} "
           f"V={w.V} kv_len sum={int(w.kv_len.sum())}", file=sys.stderr, flush=True)

@@ -25,6 +25,7 @@ namespace tv {
 namespace {
 
 constexpr int kTbThreads = 256;
+constexpr int kTbBatch = 8;                // tokens per thread whose loads are in flight together
 constexpr int kTbWaves = kTbThreads / kWave;
 constexpr int kPruneThreads = 1024;
 constexpr int kPruneSlots = 4096;          // >= 1 + k + (S - 1) k^2 for k, S <= 16
@@ -42,12 +43,6 @@ __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsig
     return a > b ? a : b;
 }
 
-__device__ __forceinline__ unsigned long long shfl_xor64(unsigned long long v, int off) {
-    const unsigned int lo = __shfl_xor((unsigned int)v, off);
-    const unsigned int hi = __shfl_xor((unsigned int)(v >> 32), off);
-    return ((unsigned long long)hi << 32) | lo;
-}
-
 __device__ __forceinline__ float key_value(unsigned long long key) {
     const unsigned int k = (unsigned int)(key >> 32);
     return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
@@ -57,18 +52,23 @@ __device__ __forceinline__ int key_index(unsigned long long key) {
     return (int)(0xFFFFFFFFu - (unsigned int)key);
 }
 
-// Running (max, sum of exp(x - max)) of one thread, fp64 sums.
+// Running (max, sum of exp(x - max)) of one thread, fp64 sums; a batch of
+// values is folded in with one rescale, without per-value branches.
 struct OnlineSum {
     float m = -__builtin_huge_valf();
     double s = 0.0;
-    __device__ __forceinline__ void add(float x) {
-        if (x == -__builtin_huge_valf()) return;        // contributes exp(-inf) = 0
-        if (x > m) {
-            s = (m == -__builtin_huge_valf()) ? 1.0 : s * exp((double)m - (double)x) + 1.0;
-            m = x;
-        } else {
-            s += exp((double)x - (double)m);
-        }
+    template <int U>
+    __device__ __forceinline__ void add_batch(const float (&x)[U], const bool (&use)[U]) {
+        float mb = m;
+        #pragma unroll
+        for (int u = 0; u < U; ++u) mb = use[u] ? fmaxf(mb, x[u]) : mb;
+        if (mb == -__builtin_huge_valf()) return;          // nothing finite so far
+        double acc = m == -__builtin_huge_valf() ? 0.0 : s * exp((double)m - (double)mb);
+        #pragma unroll
+        for (int u = 0; u < U; ++u)
+            acc += use[u] ? exp((double)x[u] - (double)mb) : 0.0;
+        s = acc;
+        m = mb;
     }
     __device__ __forceinline__ void merge(float m2, double s2) {
         if (m2 == -__builtin_huge_valf()) return;
@@ -79,45 +79,70 @@ struct OnlineSum {
     }
 };
 
-// Thread-local top-k list in registers, descending; k is a runtime value
-// <= kTbMaxK and the list is handled with fixed indices only.
-struct TopK {
-    unsigned long long t[kTbMaxK];
-    unsigned long long kmin;          // the k-th entry (0 while the list is not full)
-    __device__ __forceinline__ void init() {
-        #pragma unroll
-        for (int j = 0; j < kTbMaxK; ++j) t[j] = 0ull;
-        kmin = 0ull;
+// Cross-lane helpers without LDS: readlane (wave-uniform source lane) and a
+// one-lane shift inside each row of 16 lanes (DPP row_shr:1).
+__device__ __forceinline__ unsigned long long readlane64(unsigned long long v, int src) {
+    const unsigned int lo = __builtin_amdgcn_readlane((int)(unsigned int)v, src);
+    const unsigned int hi = __builtin_amdgcn_readlane((int)(unsigned int)(v >> 32), src);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long row_shr1_64(unsigned long long v) {
+    const int lo = (int)(unsigned int)v, hi = (int)(unsigned int)(v >> 32);
+    const unsigned int nlo = __builtin_amdgcn_update_dpp(lo, lo, 0x111, 0xF, 0xF, false);
+    const unsigned int nhi = __builtin_amdgcn_update_dpp(hi, hi, 0x111, 0xF, 0xF, false);
+    return ((unsigned long long)nhi << 32) | nlo;
+}
+
+// Largest 64-bit key over the wave, by a scan of per-row maxima (no LDS).
+__device__ __forceinline__ unsigned long long wave_max64(unsigned long long v) {
+    #pragma unroll
+    for (int sh = 1; sh < 16; sh <<= 1) {        // row_shr:sh; lanes below sh keep their value
+        const int lo = (int)(unsigned int)v, hi = (int)(unsigned int)(v >> 32);
+        const unsigned int nlo = sh == 1 ? __builtin_amdgcn_update_dpp(lo, lo, 0x111, 0xF, 0xF, false)
+                               : sh == 2 ? __builtin_amdgcn_update_dpp(lo, lo, 0x112, 0xF, 0xF, false)
+                               : sh == 4 ? __builtin_amdgcn_update_dpp(lo, lo, 0x114, 0xF, 0xF, false)
+                                         : __builtin_amdgcn_update_dpp(lo, lo, 0x118, 0xF, 0xF, false);
+        const unsigned int nhi = sh == 1 ? __builtin_amdgcn_update_dpp(hi, hi, 0x111, 0xF, 0xF, false)
+                               : sh == 2 ? __builtin_amdgcn_update_dpp(hi, hi, 0x112, 0xF, 0xF, false)
+                               : sh == 4 ? __builtin_amdgcn_update_dpp(hi, hi, 0x114, 0xF, 0xF, false)
+                                         : __builtin_amdgcn_update_dpp(hi, hi, 0x118, 0xF, 0xF, false);
+        v = umax64(v, ((unsigned long long)nhi << 32) | nlo);
     }
-    __device__ __forceinline__ void insert(unsigned long long key, int k) {
-        if (key <= kmin) return;
-        #pragma unroll
-        for (int j = 0; j < kTbMaxK; ++j) {
-            if (j < k && key > t[j]) {
-                const unsigned long long tmp = t[j];
-                t[j] = key;
-                key = tmp;
-            }
+    // lane 15 of every row now holds its row's maximum
+    return umax64(umax64(readlane64(v, 15), readlane64(v, 31)),
+                  umax64(readlane64(v, 47), readlane64(v, 63)));
+}
+
+// A wave's top-k list, distributed over lanes: lane j < k holds the (j+1)-th
+// largest key seen by the wave (0 = empty). The k-th key is the wave's
+// admission threshold, so after the first few batches almost no candidate
+// needs more than one compare; an admitted key is inserted by one shift.
+struct WaveTopK {
+    unsigned long long w = 0ull;      // this lane's entry
+    unsigned long long thr = 0ull;    // the k-th entry (wave-uniform)
+    __device__ __forceinline__ void offer(unsigned long long cand, int k, int lane) {
+        unsigned long long mask = __ballot(cand > thr);
+        while (mask) {                                   // wave-uniform
+            const int src = __builtin_ctzll(mask);
+            const unsigned long long cc = readlane64(cand, src);
+            const int pos = __popcll(__ballot(lane < k && w > cc));   // entries above cc
+            const unsigned long long up = row_shr1_64(w);
+            if (lane < k) w = lane == pos ? cc : (lane > pos ? up : w);
+            thr = readlane64(w, k - 1);
+            mask &= ~(1ull << src);
+            mask &= __ballot(cand > thr);
         }
-        unsigned long long km = 0ull;
-        #pragma unroll
-        for (int j = 0; j < kTbMaxK; ++j) km = (j == k - 1) ? t[j] : km;
-        kmin = km;
-    }
-    __device__ __forceinline__ void pop_front() {
-        #pragma unroll
-        for (int j = 0; j < kTbMaxK - 1; ++j) t[j] = t[j + 1];
-        t[kTbMaxK - 1] = 0ull;
     }
 };
 
-// Workgroup reduction of every thread's (OnlineSum, TopK) into one TbPart.
-__device__ void block_reduce_part(OnlineSum os, TopK &tk, int k, TbPart *out) {
+// Workgroup reduction of every thread's OnlineSum and every wave's top-k list
+// into one TbPart.
+__device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPart *out) {
     __shared__ float s_m[kTbWaves];
     __shared__ double s_s[kTbWaves];
-    __shared__ unsigned long long s_key[kTbWaves];
+    __shared__ unsigned long long s_key[kTbWaves * kTbMaxK];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-    // (max, sum)
     #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         const float m2 = __shfl_xor(os.m, off);
@@ -125,55 +150,88 @@ __device__ void block_reduce_part(OnlineSum os, TopK &tk, int k, TbPart *out) {
         os.merge(m2, s2);
     }
     if (lane == 0) { s_m[wave] = os.m; s_s[wave] = os.s; }
+    if (lane < kTbMaxK) s_key[wave * kTbMaxK + lane] = lane < k ? tk.w : 0ull;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        OnlineSum t;
-        for (int w = 0; w < kTbWaves; ++w) t.merge(s_m[w], s_s[w]);
-        out->m = t.m;
-        out->pad = 0;
-        out->s = t.s;
+    if (wave == 0) {
+        // the k largest of the waves' lists: one candidate per lane
+        unsigned long long c = lane < kTbWaves * kTbMaxK ? s_key[lane] : 0ull;
+        for (int r = 0; r < k; ++r) {
+            const unsigned long long best = wave_max64(c);
+            if (c == best) c = 0ull;
+            if (lane == 0) out->key[r] = best;
+        }
+        if (lane == 0) {
+            for (int r = k; r < kTbMaxK; ++r) out->key[r] = 0ull;
+            OnlineSum t;
+            for (int w = 0; w < kTbWaves; ++w) t.merge(s_m[w], s_s[w]);
+            out->m = t.m;
+            out->pad = 0;
+            out->s = t.s;
+        }
     }
-    // top-k: k rounds, each takes the largest head and pops it from its owner
-    for (int r = 0; r < k; ++r) {
-        unsigned long long best = tk.t[0];
-        #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) best = umax64(best, shfl_xor64(best, off));
-        __syncthreads();                         // s_key of the previous round is consumed
-        if (lane == 0) s_key[wave] = best;
-        __syncthreads();
-        unsigned long long top = s_key[0];
-        #pragma unroll
-        for (int w = 1; w < kTbWaves; ++w) top = umax64(top, s_key[w]);
-        if (top != 0ull && tk.t[0] == top) tk.pop_front();
-        if (threadIdx.x == 0) out->key[r] = top;
-    }
-    if (threadIdx.x == 0)
-        for (int r = k; r < kTbMaxK; ++r) out->key[r] = 0ull;
 }
 
 // Node-independent part of every (sequence, step): the non-hot tokens of the
 // step's logits, one segment of the vocabulary per workgroup. Workgroup
 // (row (b, 0), segment 0) also places the root and the first frontier.
 __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
-    const float *__restrict__ logits, const int32_t *__restrict__ hot_index,
-    const int32_t *__restrict__ root_token, int S, int V, int H, int k, int seg_len,
-    TbPart *__restrict__ rows, int max_nodes, int32_t *__restrict__ node_tok,
-    int32_t *__restrict__ node_par, double *__restrict__ node_joint,
-    int32_t *__restrict__ frontier) {
+    const float *__restrict__ logits, const int32_t *__restrict__ hot_vocab,
+    const int32_t *__restrict__ hot_index, const int32_t *__restrict__ root_token, int S, int V,
+    int H, int k, int seg_len, TbPart *__restrict__ rows, float *__restrict__ hot_logits,
+    int max_nodes, int32_t *__restrict__ node_tok, int32_t *__restrict__ node_par,
+    double *__restrict__ node_joint, int32_t *__restrict__ frontier) {
     const int row = blockIdx.x, seg = blockIdx.y;
     const int v0 = seg * seg_len, v1 = min(V, v0 + seg_len);
     const float *l = logits + (size_t)row * V;
     OnlineSum os;
-    TopK tk;
-    tk.init();
-    for (int v = v0 + threadIdx.x; v < v1; v += kTbThreads) {
-        const int h = H > 0 ? hot_index[v] : -1;
-        if (h >= 0 && h < H) continue;             // hot: handled per frontier node
-        const float x = l[v];
-        os.add(x);
-        tk.insert(pack_key(order_key(x), (unsigned int)v), k);
+    WaveTopK tk;
+    const int lane = threadIdx.x & (kWave - 1);
+    // Batches of kTbBatch tokens per thread: all loads of a batch are issued
+    // before any is used. The batch loop is uniform over the workgroup (the
+    // wave's top-k list is updated by whole-wave steps).
+    const int iters = (max(v1 - v0, 0) + kTbThreads - 1) / kTbThreads;
+    // the loads of batch n+1 are issued before batch n is used
+    int hn[kTbBatch];
+    float xn[kTbBatch];
+    auto load = [&](int it0) {
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u) {     // unconditional loads (index clamped)
+            const int v = min(v0 + (it0 + u) * kTbThreads + (int)threadIdx.x, v1 - 1);
+            hn[u] = H > 0 ? hot_index[v] : -1;
+            xn[u] = l[v];
+        }
+    };
+    if (iters > 0) load(0);
+    for (int it0 = 0; it0 < iters; it0 += kTbBatch) {
+        int hv[kTbBatch];
+        float xv[kTbBatch];
+        bool use[kTbBatch];
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u) { hv[u] = hn[u]; xv[u] = xn[u]; }
+        if (it0 + kTbBatch < iters) load(it0 + kTbBatch);
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u) {     // outside, or hot (handled per node): unused
+            const int v = v0 + (it0 + u) * kTbThreads + (int)threadIdx.x;
+            use[u] = v < v1 && !(hv[u] >= 0 && hv[u] < H) && xv[u] != -__builtin_huge_valf();
+        }
+        os.add_batch(xv, use);
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u) {
+            const int v = v0 + (it0 + u) * kTbThreads + (int)threadIdx.x;
+            tk.offer(use[u] ? pack_key(order_key(xv[u]), (unsigned int)v) : 0ull, k, lane);
+        }
     }
     block_reduce_part(os, tk, k, rows + (size_t)row * gridDim.y + seg);
+    // this row's logits of the hot tokens, contiguous for the per-node passes
+    if (H > 0) {
+        const int c_len = (H + gridDim.y - 1) / gridDim.y;
+        const int c0 = seg * c_len, c1 = min(H, c0 + c_len);
+        float *lh = hot_logits + (size_t)row * H;
+        for (int c = c0 + threadIdx.x; c < c1; c += kTbThreads) {
+            const int v = hot_vocab[c];
+            lh[c] = (v >= 0 && v < V) ? l[v] : -__builtin_huge_valf();
+        }
+    }
     if (seg == 0 && row % S == 0 && threadIdx.x == 0) {
         const int b = row / S;
         node_tok[(size_t)b * max_nodes] = root_token[b];
@@ -187,7 +245,7 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
 // Hot columns of step i for frontier slot j of sequence b, one chunk of the
 // columns per workgroup: x = l_i[hot[c]] + table[row of the node's token][c].
 __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
-    const float *__restrict__ logits, const uint16_t *__restrict__ table,
+    const float *__restrict__ hot_logits, const uint16_t *__restrict__ table,
     const int32_t *__restrict__ hot_vocab, const int32_t *__restrict__ hot_index, int S, int V,
     int H, int k, int step, int chunk_len, const int32_t *__restrict__ node_tok, int max_nodes,
     const int32_t *__restrict__ frontier, TbPart *__restrict__ parts) {
@@ -198,58 +256,80 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
     const int t = node_tok[(size_t)b * max_nodes + fr[1 + j]];
     int h = (t >= 0 && t < V) ? hot_index[t] : -1;
     if (h >= H) h = -1;
-    const float *l = logits + ((size_t)b * S + step) * V;
-    const uint16_t *r = h >= 0 ? table + (size_t)h * H : nullptr;
+    const float *lh = hot_logits + ((size_t)b * S + step) * H;
+    const uint16_t *r = table + (size_t)max(h, 0) * H;   // row 0 stands in when h < 0 (unused)
     const int c0 = c * chunk_len, c1 = min(H, c0 + chunk_len);
     OnlineSum os;
-    TopK tk;
-    tk.init();
-    for (int cc = c0 + threadIdx.x; cc < c1; cc += kTbThreads) {
-        const int v = hot_vocab[cc];
-        if (v < 0 || v >= V) continue;
-        float x = l[v];
-        if (r) x += __uint_as_float((unsigned int)r[cc] << 16);
-        os.add(x);
-        tk.insert(pack_key(order_key(x), (unsigned int)v), k);
+    WaveTopK tk;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int iters = (max(c1 - c0, 0) + kTbThreads - 1) / kTbThreads;   // batches as above
+    int vn[kTbBatch];
+    float xn[kTbBatch];
+    unsigned int rn[kTbBatch];
+    auto load = [&](int it0) {
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u) {     // unconditional loads (index clamped)
+            const int cc = min(c0 + (it0 + u) * kTbThreads + (int)threadIdx.x, c1 - 1);
+            vn[u] = hot_vocab[cc];
+            xn[u] = lh[cc];
+            rn[u] = r[cc];
+        }
+    };
+    if (iters > 0) load(0);
+    for (int it0 = 0; it0 < iters; it0 += kTbBatch) {
+        int vv[kTbBatch];
+        float xv[kTbBatch];
+        unsigned int rv[kTbBatch];
+        bool use[kTbBatch];
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u) { vv[u] = vn[u]; xv[u] = xn[u]; rv[u] = rn[u]; }
+        if (it0 + kTbBatch < iters) load(it0 + kTbBatch);
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u) {
+            const int cc = c0 + (it0 + u) * kTbThreads + (int)threadIdx.x;
+            if (h >= 0) xv[u] += __uint_as_float(rv[u] << 16);
+            use[u] = cc < c1 && vv[u] >= 0 && vv[u] < V && xv[u] != -__builtin_huge_valf();
+        }
+        os.add_batch(xv, use);
+        #pragma unroll
+        for (int u = 0; u < kTbBatch; ++u)
+            tk.offer(use[u] ? pack_key(order_key(xv[u]), (unsigned int)vv[u]) : 0ull, k, lane);
     }
     block_reduce_part(os, tk, k, out);
 }
 
-// One workgroup per sequence: for every frontier node of step i, combine the
-// step's row partials with the node's column partials into its k children
-// (token, probability, joint probability), then choose the next frontier.
-__global__ __launch_bounds__(kTbThreads) void tb_select_kernel(
+// One workgroup per sequence, one wave per frontier node of step i: combine the
+// step's row partials with the node's column partials (all loaded at once)
+// into its k children (token, probability, joint probability), then choose
+// the next frontier.
+__global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
     const TbPart *__restrict__ rows, int segs, const TbPart *__restrict__ parts, int chunks,
     int S, int k, int step, int max_nodes, int32_t *__restrict__ node_tok,
     int32_t *__restrict__ node_par, double *__restrict__ node_joint,
     int32_t *__restrict__ frontier) {
-    constexpr int kCandPerLane = 16;          // (segs + chunks) * k <= (32 + 32) * 16 candidates
+    constexpr int kCandPerLane = 16;          // (segs + chunks) * k <= 64 * 16 candidates
     __shared__ double s_joint[kTbMaxK * kTbMaxK];
     const int b = blockIdx.x;
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1), j = threadIdx.x / kWave;
     int *fr = frontier + b * (kTbMaxK + 1);
     const int nf = fr[0];
     // nodes before this step: the root, then k children per frontier node of
     // every earlier step (1 at step 0, k afterwards)
     const int base = step == 0 ? 1 : 1 + k + (step - 1) * k * k;
-    const TbPart *rp = rows + ((size_t)b * S + step) * segs;
-    const int nparts = segs + chunks;
-    const int ncand = nparts * k;
-    for (int j = wave; j < nf; j += kTbWaves) {
+    if (j < nf) {
+        const TbPart *rp = rows + ((size_t)b * S + step) * segs;
         const TbPart *cp = parts + ((size_t)b * k + j) * chunks;
-        // max and denominator over all partials
-        float m = -__builtin_huge_valf();
-        for (int q = lane; q < nparts; q += kWave) m = fmaxf(m, q < segs ? rp[q].m : cp[q - segs].m);
-        #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-        double s = 0.0;
-        for (int q = lane; q < nparts; q += kWave) {
-            const TbPart &pp = q < segs ? rp[q] : cp[q - segs];
-            if (pp.m != -__builtin_huge_valf()) s += pp.s * exp((double)pp.m - (double)m);
+        const int nparts = segs + chunks;
+        const int ncand = nparts * k;
+        const int f = fr[1 + j];
+        // every load of this node is issued before any is used
+        float pm = -__builtin_huge_valf();
+        double ps = 0.0;
+        if (lane < nparts) {
+            const TbPart *pp = lane < segs ? rp + lane : cp + (lane - segs);
+            pm = pp->m;
+            ps = pp->s;
         }
-        #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-        // top-k of all candidate keys
         unsigned long long cand[kCandPerLane];
         #pragma unroll
         for (int u = 0; u < kCandPerLane; ++u) {
@@ -261,19 +341,22 @@ __global__ __launch_bounds__(kTbThreads) void tb_select_kernel(
             }
             cand[u] = key;
         }
-        const int f = fr[1 + j];
         const double pj = node_joint[(size_t)b * max_nodes + f];
+        float m = pm;
+        #pragma unroll
+        for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+        double s = pm == -__builtin_huge_valf() ? 0.0 : ps * exp((double)pm - (double)m);
+        #pragma unroll
+        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
         for (int r = 0; r < k; ++r) {
             unsigned long long best = 0ull;
             #pragma unroll
             for (int u = 0; u < kCandPerLane; ++u) best = umax64(best, cand[u]);
-            #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) best = umax64(best, shfl_xor64(best, off));
+            best = wave_max64(best);
             #pragma unroll
             for (int u = 0; u < kCandPerLane; ++u) cand[u] = cand[u] == best ? 0ull : cand[u];
             if (lane == 0) {
-                const int n = base + j * k + r;
-                const size_t at = (size_t)b * max_nodes + n;
+                const size_t at = (size_t)b * max_nodes + base + j * k + r;
                 double joint = 0.0;
                 int tok = -1;
                 if (best != 0ull) {
@@ -289,34 +372,19 @@ __global__ __launch_bounds__(kTbThreads) void tb_select_kernel(
     }
     __syncthreads();
     // next frontier: the k children of this step with the largest joint
-    // probabilities, largest first, ties to the earlier child
-    if (wave == 0) {
-        const int nc = nf * k;
-        int taken[4] = {0, 0, 0, 0};
-        for (int r = 0; r < k && r < nc; ++r) {
-            double bj = -1.0;
-            int bi = 1 << 30;
-            #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = lane + u * kWave;
-                if (i < nc && !taken[u]) {
-                    const double jv = s_joint[i];
-                    if (jv > bj || (jv == bj && i < bi)) { bj = jv; bi = i; }
-                }
-            }
-            #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) {
-                const double oj = __shfl_xor(bj, off);
-                const int oi = __shfl_xor(bi, off);
-                if (oj > bj || (oj == bj && oi < bi)) { bj = oj; bi = oi; }
-            }
-            #pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if (lane + u * kWave == bi) taken[u] = 1;
-            if (lane == 0) fr[1 + r] = base + bi;
+    // probabilities, largest first, ties to the earlier child. Child i's rank
+    // is the number of children before it in that order.
+    const int nc = nf * k;
+    for (int i = threadIdx.x; i < nc; i += kTbMaxK * kWave) {
+        const double ji = s_joint[i];
+        int rank = 0;
+        for (int q = 0; q < nc; ++q) {
+            const double jq = s_joint[q];
+            rank += (jq > ji || (jq == ji && q < i)) ? 1 : 0;
         }
-        if (lane == 0) fr[0] = min(k, nc);
+        if (rank < k) fr[1 + rank] = base + i;
     }
+    if (threadIdx.x == 0) fr[0] = min(k, nc);
 }
 
 // One workgroup per sequence: keep the `budget` nodes of largest joint
@@ -409,19 +477,16 @@ __global__ __launch_bounds__(kPruneThreads) void tb_prune_kernel(
 TreeBuildPlan tree_build_plan(int B, int S, int V, int H, int k) {
     TreeBuildPlan pl;
     const long rows = (long)B * S;
-    long segs = rows > 0 ? (2048 + rows - 1) / rows : 1;
-    const long max_segs = ((long)V + 2047) / 2048;
-    if (segs > max_segs) segs = max_segs;
+    // at least 16384 tokens per workgroup (64 per thread), so that the top-k
+    // filter, not the insertions, sets the cost per token
+    long segs = ((long)V + 16383) / 16384;
     if (segs > 32) segs = 32;
     if (segs < 1) segs = 1;
     pl.segs = (int)segs;
     pl.seg_len = (int)(((long)V + segs - 1) / segs);
     long chunks = 0;
     if (H > 0) {
-        const long slots = (long)B * k;
-        chunks = slots > 0 ? (1024 + slots - 1) / slots : 1;
-        const long max_chunks = ((long)H + 255) / 256;
-        if (chunks > max_chunks) chunks = max_chunks;
+        chunks = ((long)H + 8191) / 8192;            // at least 8192 columns per workgroup
         if (chunks > 32) chunks = 32;
         if (chunks < 1) chunks = 1;
     }
@@ -429,6 +494,7 @@ TreeBuildPlan tree_build_plan(int B, int S, int V, int H, int k) {
     pl.chunk_len = chunks > 0 ? (int)(((long)H + chunks - 1) / chunks) : 0;
     pl.max_nodes = 1 + k + (S - 1) * k * k;
     pl.rows_bytes = (size_t)rows * segs * sizeof(TbPart);
+    pl.hot_logits_bytes = (size_t)rows * H * sizeof(float);
     pl.parts_bytes = (size_t)B * k * (chunks > 0 ? chunks : 1) * sizeof(TbPart);
     pl.nodes_bytes = (size_t)B * pl.max_nodes * (2 * sizeof(int32_t) + sizeof(double));
     pl.frontier_bytes = (size_t)B * (kTbMaxK + 1) * sizeof(int32_t);
@@ -450,6 +516,7 @@ hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
     };
     TbPart *rows = reinterpret_cast<TbPart *>(carve(pl.rows_bytes));
     TbPart *parts = reinterpret_cast<TbPart *>(carve(pl.parts_bytes));
+    float *hot_logits = reinterpret_cast<float *>(carve(pl.hot_logits_bytes));
     const size_t nn = (size_t)B * pl.max_nodes;
     int32_t *node_tok = reinterpret_cast<int32_t *>(carve(nn * sizeof(int32_t)));
     int32_t *node_par = reinterpret_cast<int32_t *>(carve(nn * sizeof(int32_t)));
@@ -457,15 +524,15 @@ hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
     int32_t *frontier = reinterpret_cast<int32_t *>(carve(pl.frontier_bytes));
 
     hipError_t e = launch_kernel(tb_rows_kernel, dim3(B * S, pl.segs), dim3(kTbThreads), s, logits,
-                                 hot_index, root_token, S, V, H, k, pl.seg_len, rows, pl.max_nodes,
-                                 node_tok, node_par, node_joint, frontier);
+                                 hot_vocab, hot_index, root_token, S, V, H, k, pl.seg_len, rows,
+                                 hot_logits, pl.max_nodes, node_tok, node_par, node_joint, frontier);
     for (int i = 0; i < S && e == hipSuccess; ++i) {
         if (pl.chunks > 0)
-            e = launch_kernel(tb_expand_kernel, dim3(B, k, pl.chunks), dim3(kTbThreads), s, logits,
-                              table, hot_vocab, hot_index, S, V, H, k, i, pl.chunk_len, node_tok,
-                              pl.max_nodes, frontier, parts);
+            e = launch_kernel(tb_expand_kernel, dim3(B, k, pl.chunks), dim3(kTbThreads), s,
+                              hot_logits, table, hot_vocab, hot_index, S, V, H, k, i,
+                              pl.chunk_len, node_tok, pl.max_nodes, frontier, parts);
         if (e == hipSuccess)
-            e = launch_kernel(tb_select_kernel, dim3(B), dim3(kTbThreads), s, rows, pl.segs, parts,
+            e = launch_kernel(tb_select_kernel, dim3(B), dim3(kTbMaxK * kWave), s, rows, pl.segs, parts,
                               pl.chunks, S, k, i, pl.max_nodes, node_tok, node_par, node_joint,
                               frontier);
     }

@@ -269,6 +269,7 @@ size_t tv_tree_build_workspace_size(int B, int S, int V, int H, int k) {
     const tv::TreeBuildPlan pl = tv::tree_build_plan(B, S, V, H, k);
     const size_t nn = (size_t)B * pl.max_nodes;
     return round_up(pl.rows_bytes, 256) + round_up(pl.parts_bytes, 256) +
+           round_up(pl.hot_logits_bytes, 256) +
            2 * round_up(nn * sizeof(int32_t), 256) + round_up(nn * sizeof(double), 256) +
            round_up(pl.frontier_bytes, 256) + 256;
 }

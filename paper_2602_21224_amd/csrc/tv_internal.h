@@ -49,7 +49,7 @@ struct TreeBuildPlan {
     int segs, seg_len;         // vocabulary segments per (sequence, step) row
     int chunks, chunk_len;     // hot-column chunks per frontier node (0 without hot tokens)
     int max_nodes;             // nodes of the unpruned tree: 1 + k + (S - 1) k^2
-    size_t rows_bytes, parts_bytes, nodes_bytes, frontier_bytes;
+    size_t rows_bytes, parts_bytes, hot_logits_bytes, nodes_bytes, frontier_bytes;
 };
 TreeBuildPlan tree_build_plan(int B, int S, int V, int H, int k);
 
