@@ -201,4 +201,4 @@ def kv_compact(k_tree, v_tree, k_cache, v_cache, page_table, kv_len, accept_idx,
     return kc, vc
 
 
-from .tree_build import tree_build  # noqa: E402  (Alg. 1 + budget pruning, numpy)
+from .tree_build import resample, tree_build  # noqa: E402  (Alg. 1, Alg. 2, pruning; numpy)

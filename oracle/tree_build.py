@@ -134,3 +134,42 @@ def tree_build(logits, root, table_bits, hot, k: int, budget: int, margins: list
             margins.append((js[budget - 1] - js[budget]) / js[budget - 1])
         par[b], tok[b], jnt[b], nn[b] = prune(t, p, j, budget)
     return par, tok, jnt, nn
+
+
+def resample(logits, bonus, accept_len, table_bits, hot, k: int, r: int, budget: int,
+             margins: list | None = None):
+    """Re-sampling (Alg. 2, §5.3) for a batch after verification.
+
+    The ground-truth token is the verification's bonus token; the first
+    rejected draft position is accept_len (the accepted path counts the root at
+    depth 0, so the token at depth accept_len was rejected and was drawn from
+    logits row accept_len - 1). The remaining logits are rows accept_len ..
+    S-1 and N_remain = S - accept_len. If N_remain > r the new tree is
+    BuildSubtree(remaining logits, bonus, k, N_remain), pruned to the budget
+    like a first tree; otherwise it is the single ground-truth node. A sequence
+    that verified nothing (accept_len 0) gets an empty tree.
+    Returns parent, token, joint, num_nodes as tree_build does.
+    """
+    logits = np.asarray(logits, dtype=np.float32)
+    B, S, _ = logits.shape
+    table = np.asarray(table_bits, dtype=np.uint16)
+    hot = np.asarray(hot, dtype=np.int64)
+    par = np.full((B, budget), -1, dtype=np.int32)
+    tok = np.full((B, budget), -1, dtype=np.int32)
+    jnt = np.zeros((B, budget), dtype=np.float64)
+    nn = np.zeros(B, dtype=np.int32)
+    for b in range(B):
+        a = int(accept_len[b])
+        if a <= 0:
+            continue
+        n_remain = S - a
+        if n_remain > r:
+            t, p, _, j = build_tree_one(logits[b, a:], int(bonus[b]), table, hot, k, margins)
+            if margins is not None and len(j) > budget:
+                js = sorted(j, reverse=True)
+                margins.append((js[budget - 1] - js[budget]) / js[budget - 1])
+            par[b], tok[b], jnt[b], nn[b] = prune(t, p, j, budget)
+        else:
+            tok[b, 0], jnt[b, 0], nn[b] = int(bonus[b]), 1.0, 1
+    return par, tok, jnt, nn
+

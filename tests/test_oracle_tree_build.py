@@ -225,3 +225,64 @@ def test_budget_pruning(budget):
         if dropped:
             assert kept[0] >= max(j[i] for i in dropped)
         assert sorted(j, reverse=True)[:n] == pytest.approx(sorted(kept, reverse=True), rel=0)
+
+
+# ---------------------------------------------------------------- re-sampling (Alg. 2, §5.3)
+def resample_narrative():
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                    "resample_narrative.json")))
+    vocab = g["vocab"]
+    ids = {t: i for i, t in enumerate(vocab)}
+    V, S = len(vocab), len(g["steps"])
+    logits = np.full((1, S, V), -1e4, dtype=np.float32)
+    table = np.zeros((V, V), dtype=np.float32)
+    for i, st in enumerate(g["steps"]):
+        for t, p in st["logits"].items():
+            logits[0, i, ids[t]] = np.float32(np.log(p))
+        for row, visible in st["masks"].items():
+            table[ids[row]] = g["mask_value"]
+            for t in visible:
+                table[ids[row], ids[t]] = 0.0
+    return g, ids, logits, f32_to_bf16_bits(table), np.arange(V, dtype=np.int32)
+
+
+def test_resample_narrative():
+    g, ids, logits, table, hot = resample_narrative()
+    par, tok, jnt, nn = oracle.resample(logits, np.array([ids[g["bonus"]]], np.int32),
+                                        np.array([g["accept_len"]], np.int32), table, hot,
+                                        g["k"], g["r"], 16)
+    names = g["vocab"]
+    assert nn[0] == len(g["expected_nodes"])
+    for n, (t, p_name, jp) in enumerate(g["expected_nodes"]):
+        assert names[tok[0, n]] == t, (n, names[tok[0, n]], t)
+        assert (par[0, n] < 0) == (p_name is None)
+        if p_name is not None:
+            assert names[tok[0, par[0, n]]] == p_name
+        assert jnt[0, n] == pytest.approx(jp, rel=1e-6)
+
+
+def test_resample_threshold_and_empty():
+    """N_remain = S - accept_len; at or below r the new tree is the single
+    ground-truth node; a sequence that verified nothing gets no tree."""
+    logits, root, table, hot = random_case(44, B=4, S=5)
+    bonus = np.array([3, 4, 5, 6], np.int32)
+    alen = np.array([0, 3, 4, 6], np.int32)          # N_remain: -, 2, 1, -1
+    par, tok, jnt, nn = oracle.resample(logits, bonus, alen, table, hot, 2, 1, 20)
+    assert nn.tolist() == [0, 1 + 2 + 4, 1, 1]
+    assert (tok[0] == -1).all() and (par[0] == -1).all()
+    assert tok[2, 0] == 5 and jnt[2, 0] == 1.0 and (tok[2, 1:] == -1).all()
+    assert tok[3, 0] == 6 and par[3, 0] == -1
+
+
+def test_resample_uses_the_remaining_logits():
+    """The re-sampled tree of a sequence with accept_len a is the tree the
+    builder draws from logits rows a..S-1 with the bonus token as root."""
+    logits, root, table, hot = random_case(45, B=3, S=6)
+    bonus = np.array([7, 8, 9], np.int32)
+    alen = np.array([1, 2, 4], np.int32)
+    got = oracle.resample(logits, bonus, alen, table, hot, 3, 0, 30)
+    for b in range(3):
+        a = int(alen[b])
+        want = oracle.tree_build(logits[b:b + 1, a:], bonus[b:b + 1], table, hot, 3, 30)
+        for x, y in zip(got, want):
+            np.testing.assert_array_equal(x[b], y[0])
