@@ -272,6 +272,34 @@ TV_API int tv_validate_inputs(const int32_t *page_table, const int32_t *kv_len,
  * inputs that break the contract are unspecified.
  * ------------------------------------------------------------------------ */
 TV_API size_t tv_tree_build_workspace_size(int B, int S, int V, int H, int k);
+
+/* ------------------------------------------------------------------------
+ * tree_resample  (re-sampling after verification, Alg. 2 of §5.3)
+ *
+ * The draft logits of the rejected steps are reused with the verified token's
+ * information: for each sequence b, bonus_token[b] (the verification's bonus
+ * token, i.e. the ground truth at the first rejected position) roots a new
+ * tree. The first rejected position is accept_len[b] (the accepted path of
+ * tree_argmax_accept counts the root, so the token at depth accept_len[b] was
+ * rejected); the remaining logits are rows accept_len[b] .. S-1 of
+ * logits[b], N_remain = S - accept_len[b]. If N_remain > r the tree is built
+ * from them exactly as tree_build builds a tree (same token-info table, k,
+ * pruning to `budget`); otherwise it is the single node bonus_token[b].
+ * A sequence with accept_len[b] <= 0 verified nothing and gets no tree
+ * (num_nodes[b] = 0, all slots padding). The output feeds the next
+ * verification, e.g. as the second root of a fused forest.
+ *
+ *   bonus_token, accept_len   [B] int32 (device), as tree_argmax_accept wrote them
+ *   r                         re-sampling threshold, >= 0
+ * Everything else, the limits and the workspace (tv_tree_build_workspace_size)
+ * are those of tree_build.
+ * ------------------------------------------------------------------------ */
+TV_API int tree_resample(const float *logits, const int32_t *bonus_token,
+                         const int32_t *accept_len, const uint16_t *token_info,
+                         const int32_t *hot_vocab, const int32_t *hot_index, int B, int S, int V,
+                         int H, int k, int r, int budget, int32_t *parent, int32_t *token,
+                         float *joint, int32_t *num_nodes, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream);
 TV_API int tree_build(const float *logits, const int32_t *root_token, const uint16_t *token_info,
                       const int32_t *hot_vocab, const int32_t *hot_index, int B, int S, int V,
                       int H, int k, int budget, int32_t *parent, int32_t *token, float *joint,

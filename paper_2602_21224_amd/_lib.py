@@ -54,6 +54,8 @@ def load():
     lib.tv_tree_build_workspace_size.restype = sz
     lib.tree_build.argtypes = [p] * 5 + [i] * 6 + [p] * 5 + [sz, p]
     lib.tree_build.restype = i
+    lib.tree_resample.argtypes = [p] * 6 + [i] * 7 + [p] * 5 + [sz, p]
+    lib.tree_resample.restype = i
     _lib = lib
     return lib
 
@@ -254,5 +256,44 @@ def tree_build(logits, root_token, token_info, hot_vocab, hot_index, *, k: int, 
         budget, _ptr(parent), _ptr(token), _ptr(joint), _ptr(num_nodes), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "tree_build")
+    return parent, token, joint, num_nodes
+
+
+def tree_resample(logits, bonus_token, accept_len, token_info, hot_vocab, hot_index, *, k: int,
+                  r: int, budget: int, parent=None, token=None, joint=None, num_nodes=None,
+                  workspace=None, stream=None):
+    """Re-sampled draft trees after verification (Alg. 2): rooted at the bonus
+    tokens, drawn from logits rows accept_len .. S-1 when more than r remain.
+    Same tensors and outputs as tree_build, plus bonus_token / accept_len [B]."""
+    B, S, V = logits.shape
+    _want(logits, "logits", (torch.float32,))
+    _want(bonus_token, "bonus_token", (torch.int32,), (B,))
+    _want(accept_len, "accept_len", (torch.int32,), (B,))
+    H = 0 if token_info is None else token_info.shape[0]
+    if H > 0:
+        _want(token_info, "token_info", _BF16, (H, H))
+        _want(hot_vocab, "hot_vocab", (torch.int32,), (H,))
+        _want(hot_index, "hot_index", (torch.int32,), (V,))
+    dev = logits.device
+    mk = lambda shape, dt: torch.empty(shape, dtype=dt, device=dev)
+    parent = mk((B, budget), torch.int32) if parent is None else parent
+    token = mk((B, budget), torch.int32) if token is None else token
+    joint = mk((B, budget), torch.float32) if joint is None else joint
+    num_nodes = mk((B,), torch.int32) if num_nodes is None else num_nodes
+    _want(parent, "parent", (torch.int32,), (B, budget))
+    _want(token, "token", (torch.int32,), (B, budget))
+    _want(joint, "joint", (torch.float32,), (B, budget))
+    _want(num_nodes, "num_nodes", (torch.int32,), (B,))
+    need = tree_build_workspace_size(B, S, V, H, k)
+    if need == 0:
+        raise TreeVerifyError(f"tree_resample: unsupported shape B={B} S={S} V={V} H={H} k={k}")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    st = load().tree_resample(
+        _ptr(logits), _ptr(bonus_token), _ptr(accept_len), _ptr(token_info if H > 0 else None),
+        _ptr(hot_vocab if H > 0 else None), _ptr(hot_index if H > 0 else None), B, S, V, H, k, r,
+        budget, _ptr(parent), _ptr(token), _ptr(joint), _ptr(num_nodes), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "tree_resample")
     return parent, token, joint, num_nodes
 

@@ -171,14 +171,33 @@ __device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPar
     }
 }
 
+// Steps of sequence b: logits rows [first, first + count). A first tree uses all
+// S rows. A re-sampled tree (Alg. 2; accept_len given) starts after the first
+// rejected position -- the accepted path counts the root, so that position is
+// accept_len and the remaining rows are accept_len .. S-1 -- and is the single
+// ground-truth node unless more than r rows remain. A sequence that verified
+// nothing has no tree (count -1).
+struct TbWindow {
+    int first, count;
+};
+
+__device__ __forceinline__ TbWindow tb_window(const int32_t *accept_len, int b, int S, int r) {
+    if (!accept_len) return {0, S};
+    const int a = accept_len[b];
+    if (a <= 0) return {0, -1};
+    const int remain = S - a;
+    return {min(a, S), remain > r ? remain : 0};
+}
+
 // Node-independent part of every (sequence, step): the non-hot tokens of the
 // step's logits, one segment of the vocabulary per workgroup. Workgroup
 // (row (b, 0), segment 0) also places the root and the first frontier.
 __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
     const float *__restrict__ logits, const int32_t *__restrict__ hot_vocab,
-    const int32_t *__restrict__ hot_index, const int32_t *__restrict__ root_token, int S, int V,
-    int H, int k, int seg_len, TbPart *__restrict__ rows, float *__restrict__ hot_logits,
-    int max_nodes, int32_t *__restrict__ node_tok, int32_t *__restrict__ node_par,
+    const int32_t *__restrict__ hot_index, const int32_t *__restrict__ root_token,
+    const int32_t *__restrict__ accept_len, int r, int S, int V, int H, int k, int seg_len,
+    TbPart *__restrict__ rows, float *__restrict__ hot_logits, int max_nodes,
+    int32_t *__restrict__ node_tok, int32_t *__restrict__ node_par,
     double *__restrict__ node_joint, int32_t *__restrict__ frontier) {
     const int row = blockIdx.x, seg = blockIdx.y;
     const int v0 = seg * seg_len, v1 = min(V, v0 + seg_len);
@@ -237,7 +256,7 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
         node_tok[(size_t)b * max_nodes] = root_token[b];
         node_par[(size_t)b * max_nodes] = -1;
         node_joint[(size_t)b * max_nodes] = 1.0;
-        frontier[b * (kTbMaxK + 1)] = 1;           // count, then node ids
+        frontier[b * (kTbMaxK + 1)] = tb_window(accept_len, b, S, r).count > 0 ? 1 : 0;  // count, ids
         frontier[b * (kTbMaxK + 1) + 1] = 0;
     }
 }
@@ -246,18 +265,21 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
 // columns per workgroup: x = l_i[hot[c]] + table[row of the node's token][c].
 __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
     const float *__restrict__ hot_logits, const uint16_t *__restrict__ table,
-    const int32_t *__restrict__ hot_vocab, const int32_t *__restrict__ hot_index, int S, int V,
-    int H, int k, int step, int chunk_len, const int32_t *__restrict__ node_tok, int max_nodes,
+    const int32_t *__restrict__ hot_vocab, const int32_t *__restrict__ hot_index,
+    const int32_t *__restrict__ accept_len, int r, int S, int V, int H, int k, int step,
+    int chunk_len, const int32_t *__restrict__ node_tok, int max_nodes,
     const int32_t *__restrict__ frontier, TbPart *__restrict__ parts) {
     const int b = blockIdx.x, j = blockIdx.y, c = blockIdx.z;
     const int *fr = frontier + b * (kTbMaxK + 1);
     TbPart *out = parts + ((size_t)b * k + j) * gridDim.z + c;
+    const TbWindow win = tb_window(accept_len, b, S, r);
+    if (step >= win.count) return;                 // this sequence's tree is complete
     if (j >= fr[0]) return;                        // no such frontier node at this step
     const int t = node_tok[(size_t)b * max_nodes + fr[1 + j]];
     int h = (t >= 0 && t < V) ? hot_index[t] : -1;
     if (h >= H) h = -1;
-    const float *lh = hot_logits + ((size_t)b * S + step) * H;
-    const uint16_t *r = table + (size_t)max(h, 0) * H;   // row 0 stands in when h < 0 (unused)
+    const float *lh = hot_logits + ((size_t)b * S + win.first + step) * H;
+    const uint16_t *trow = table + (size_t)max(h, 0) * H;   // row 0 stands in when h < 0 (unused)
     const int c0 = c * chunk_len, c1 = min(H, c0 + chunk_len);
     OnlineSum os;
     WaveTopK tk;
@@ -272,7 +294,7 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
             const int cc = min(c0 + (it0 + u) * kTbThreads + (int)threadIdx.x, c1 - 1);
             vn[u] = hot_vocab[cc];
             xn[u] = lh[cc];
-            rn[u] = r[cc];
+            rn[u] = trow[cc];
         }
     };
     if (iters > 0) load(0);
@@ -304,20 +326,23 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
 // the next frontier.
 __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
     const TbPart *__restrict__ rows, int segs, const TbPart *__restrict__ parts, int chunks,
-    int S, int k, int step, int max_nodes, int32_t *__restrict__ node_tok,
+    const int32_t *__restrict__ accept_len, int r, int S, int k, int step, int max_nodes,
+    int32_t *__restrict__ node_tok,
     int32_t *__restrict__ node_par, double *__restrict__ node_joint,
     int32_t *__restrict__ frontier) {
     constexpr int kCandPerLane = 16;          // (segs + chunks) * k <= 64 * 16 candidates
     __shared__ double s_joint[kTbMaxK * kTbMaxK];
     const int b = blockIdx.x;
     const int lane = threadIdx.x & (kWave - 1), j = threadIdx.x / kWave;
+    const TbWindow win = tb_window(accept_len, b, S, r);
+    if (step >= win.count) return;                 // uniform: this sequence is done
     int *fr = frontier + b * (kTbMaxK + 1);
     const int nf = fr[0];
     // nodes before this step: the root, then k children per frontier node of
     // every earlier step (1 at step 0, k afterwards)
     const int base = step == 0 ? 1 : 1 + k + (step - 1) * k * k;
     if (j < nf) {
-        const TbPart *rp = rows + ((size_t)b * S + step) * segs;
+        const TbPart *rp = rows + ((size_t)b * S + win.first + step) * segs;
         const TbPart *cp = parts + ((size_t)b * k + j) * chunks;
         const int nparts = segs + chunks;
         const int ncand = nparts * k;
@@ -390,7 +415,8 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
 // One workgroup per sequence: keep the `budget` nodes of largest joint
 // probability (ties to the earlier node), in creation order, parents renumbered.
 __global__ __launch_bounds__(kPruneThreads) void tb_prune_kernel(
-    int n, int budget, int max_nodes, const int32_t *__restrict__ node_tok,
+    const int32_t *__restrict__ accept_len, int r, int S, int k, int budget, int max_nodes,
+    const int32_t *__restrict__ node_tok,
     const int32_t *__restrict__ node_par, const double *__restrict__ node_joint,
     int32_t *__restrict__ parent, int32_t *__restrict__ token, float *__restrict__ joint,
     int32_t *__restrict__ num_nodes) {
@@ -400,6 +426,8 @@ __global__ __launch_bounds__(kPruneThreads) void tb_prune_kernel(
     __shared__ int s_warp[kPruneThreads / kWave];
     const int b = blockIdx.x, tid = threadIdx.x;
     const size_t nb = (size_t)b * max_nodes;
+    const TbWindow win = tb_window(accept_len, b, S, r);
+    const int n = win.count < 0 ? 0 : win.count == 0 ? 1 : 1 + k + (win.count - 1) * k * k;
     int P2 = 1;
     while (P2 < n) P2 <<= 1;
     for (int i = tid; i < P2; i += kPruneThreads) {
@@ -503,9 +531,10 @@ TreeBuildPlan tree_build_plan(int B, int S, int V, int H, int k) {
 
 hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
                              const uint16_t *table, const int32_t *hot_vocab,
-                             const int32_t *hot_index, int B, int S, int V, int H, int k,
-                             int budget, int32_t *parent, int32_t *token, float *joint,
-                             int32_t *num_nodes, void *workspace, hipStream_t s) {
+                             const int32_t *hot_index, const int32_t *accept_len, int r, int B,
+                             int S, int V, int H, int k, int budget, int32_t *parent,
+                             int32_t *token, float *joint, int32_t *num_nodes, void *workspace,
+                             hipStream_t s) {
     if (B == 0) return hipSuccess;
     const TreeBuildPlan pl = tree_build_plan(B, S, V, H, k);
     char *base = static_cast<char *>(workspace);
@@ -524,22 +553,23 @@ hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
     int32_t *frontier = reinterpret_cast<int32_t *>(carve(pl.frontier_bytes));
 
     hipError_t e = launch_kernel(tb_rows_kernel, dim3(B * S, pl.segs), dim3(kTbThreads), s, logits,
-                                 hot_vocab, hot_index, root_token, S, V, H, k, pl.seg_len, rows,
-                                 hot_logits, pl.max_nodes, node_tok, node_par, node_joint, frontier);
+                                 hot_vocab, hot_index, root_token, accept_len, r, S, V, H, k,
+                                 pl.seg_len, rows, hot_logits, pl.max_nodes, node_tok, node_par,
+                                 node_joint, frontier);
     for (int i = 0; i < S && e == hipSuccess; ++i) {
         if (pl.chunks > 0)
             e = launch_kernel(tb_expand_kernel, dim3(B, k, pl.chunks), dim3(kTbThreads), s,
-                              hot_logits, table, hot_vocab, hot_index, S, V, H, k, i,
-                              pl.chunk_len, node_tok, pl.max_nodes, frontier, parts);
+                              hot_logits, table, hot_vocab, hot_index, accept_len, r, S, V, H, k,
+                              i, pl.chunk_len, node_tok, pl.max_nodes, frontier, parts);
         if (e == hipSuccess)
-            e = launch_kernel(tb_select_kernel, dim3(B), dim3(kTbMaxK * kWave), s, rows, pl.segs, parts,
-                              pl.chunks, S, k, i, pl.max_nodes, node_tok, node_par, node_joint,
-                              frontier);
+            e = launch_kernel(tb_select_kernel, dim3(B), dim3(kTbMaxK * kWave), s, rows, pl.segs,
+                              parts, pl.chunks, accept_len, r, S, k, i, pl.max_nodes, node_tok,
+                              node_par, node_joint, frontier);
     }
     if (e == hipSuccess)
-        e = launch_kernel(tb_prune_kernel, dim3(B), dim3(kPruneThreads), s, pl.max_nodes, budget,
-                          pl.max_nodes, node_tok, node_par, node_joint, parent, token, joint,
-                          num_nodes);
+        e = launch_kernel(tb_prune_kernel, dim3(B), dim3(kPruneThreads), s, accept_len, r, S, k,
+                          budget, pl.max_nodes, node_tok, node_par, node_joint, parent, token,
+                          joint, num_nodes);
     return e;
 }
 

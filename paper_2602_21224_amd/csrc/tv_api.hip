@@ -289,8 +289,31 @@ int tree_build(const float *logits, const int32_t *root_token, const uint16_t *t
     if (workspace_bytes < tv_tree_build_workspace_size(B, S, V, H, k)) return TV_ERR_WORKSPACE;
     if (!device_ok()) return TV_ERR_DEVICE;
     const hipError_t e = tv::launch_tree_build(logits, root_token, token_info, hot_vocab,
-                                               hot_index, B, S, V, H, k, budget, parent, token,
-                                               joint, num_nodes, workspace, stream);
+                                               hot_index, nullptr, 0, B, S, V, H, k, budget,
+                                               parent, token, joint, num_nodes, workspace,
+                                               stream);
+    return e == hipSuccess ? TV_OK : TV_ERR_HIP;
+}
+
+int tree_resample(const float *logits, const int32_t *bonus_token, const int32_t *accept_len,
+                  const uint16_t *token_info, const int32_t *hot_vocab, const int32_t *hot_index,
+                  int B, int S, int V, int H, int k, int r, int budget, int32_t *parent,
+                  int32_t *token, float *joint, int32_t *num_nodes, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream) {
+    if (!tree_build_shape_ok(B, S, V, H, k) || budget < 1 || budget > tv::kMaxNodes || r < 0)
+        return TV_ERR_SHAPE;
+    if (B == 0) return TV_OK;
+    if (!logits || !bonus_token || !accept_len || !parent || !token || !joint || !num_nodes ||
+        !workspace || (H > 0 && (!token_info || !hot_vocab || !hot_index)))
+        return TV_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(logits) & 3u) || (reinterpret_cast<uintptr_t>(workspace) & 7u))
+        return TV_ERR_ALIGN;
+    if (workspace_bytes < tv_tree_build_workspace_size(B, S, V, H, k)) return TV_ERR_WORKSPACE;
+    if (!device_ok()) return TV_ERR_DEVICE;
+    const hipError_t e = tv::launch_tree_build(logits, bonus_token, token_info, hot_vocab,
+                                               hot_index, accept_len, r, B, S, V, H, k, budget,
+                                               parent, token, joint, num_nodes, workspace,
+                                               stream);
     return e == hipSuccess ? TV_OK : TV_ERR_HIP;
 }
 

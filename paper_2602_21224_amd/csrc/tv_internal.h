@@ -101,9 +101,10 @@ inline hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block,
 // Host-side launchers (defined next to their kernels).
 hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
                              const uint16_t *table, const int32_t *hot_vocab,
-                             const int32_t *hot_index, int B, int S, int V, int H, int k,
-                             int budget, int32_t *parent, int32_t *token, float *joint,
-                             int32_t *num_nodes, void *workspace, hipStream_t s);
+                             const int32_t *hot_index, const int32_t *accept_len, int r, int B,
+                             int S, int V, int H, int k, int budget, int32_t *parent,
+                             int32_t *token, float *joint, int32_t *num_nodes, void *workspace,
+                             hipStream_t s);
 hipError_t launch_tree_attention(const AttnParams &p, int head_dim, int waves, hipStream_t s);
 hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const int32_t *parent,
                                 const int32_t *num_nodes, int B, int N, int V, int segs,

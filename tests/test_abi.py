@@ -137,3 +137,16 @@ def test_tree_build_argument_checks(lib):
     assert need > 0 and tb(lib, ws_bytes=need - 1) == -4
     assert lib.tv_tree_build_workspace_size(2, 0, 1000, 100, 4) == 0
 
+
+def test_tree_resample_argument_checks(lib):
+    def rs(**kw):
+        a = dict(logits=FAKE, bonus=FAKE, alen=FAKE, table=FAKE, hot_vocab=FAKE, hot_index=FAKE,
+                 B=2, S=4, V=1000, H=100, k=4, r=1, budget=32, parent=FAKE, token=FAKE,
+                 joint=FAKE, num_nodes=FAKE, ws=FAKE, ws_bytes=1 << 40)
+        a.update(kw)
+        return lib.tree_resample(*a.values(), STREAM)
+    assert rs(B=0) == 0
+    assert rs(bonus=NULL) == -1 and rs(alen=NULL) == -1
+    assert rs(r=-1) == -2 and rs(S=17) == -2 and rs(budget=0) == -2
+    assert rs(ws_bytes=lib.tv_tree_build_workspace_size(2, 4, 1000, 100, 4) - 1) == -4
+

@@ -124,3 +124,94 @@ def test_tree_build_reuses_workspace(oracle_mod):
         np.testing.assert_array_equal(tok.cpu().numpy(), want[1])
         np.testing.assert_array_equal(par.cpu().numpy(), want[0])
         np.testing.assert_array_equal(nn.cpu().numpy(), want[3])
+
+
+# ---------------------------------------------------------------- re-sampling (Alg. 2)
+def run_resample(T, x, bonus, alen, r, budget=None, k=None):
+    budget = x.budget if budget is None else budget
+    k = x.k if k is None else k
+    H = x.H
+    tab = U.dev(x.table.view(np.int16)).view(torch.bfloat16) if H > 0 else None
+    out = T.tree_resample(U.dev(x.logits), U.dev(bonus), U.dev(alen), tab,
+                          U.dev(x.hot_vocab) if H > 0 else None,
+                          U.dev(x.hot_index) if H > 0 else None, k=k, r=r, budget=budget)
+    torch.cuda.synchronize()
+    return [t.cpu().numpy() for t in out]
+
+
+def compare_resample(oracle_mod, T, x, bonus, alen, r, label):
+    print(f"case {label}: B={x.B} S={x.S} V={x.V} H={x.H} k={x.k} r={r} "
+          f"accept_len={alen.tolist()}", flush=True)
+    margins = []
+    want = oracle_mod.resample(x.logits, bonus, alen, x.table, x.hot_vocab, x.k, r, x.budget,
+                               margins)
+    if margins:
+        assert min(margins) > 1e-9, f"{label}: near-tie in the oracle ({min(margins):.2e})"
+    got = run_resample(T, x, bonus, alen, r)
+    np.testing.assert_array_equal(got[3], want[3], err_msg=f"{label} num_nodes")
+    np.testing.assert_array_equal(got[1], want[1], err_msg=f"{label} token")
+    np.testing.assert_array_equal(got[0], want[0], err_msg=f"{label} parent")
+    np.testing.assert_allclose(got[2], want[2], rtol=1e-6, atol=0, err_msg=f"{label} joint")
+    return got
+
+
+@pytest.mark.parametrize("case", range(3))
+def test_resample_cases(oracle_mod, case):
+    T = U.require_gpu()
+    B, S, V, H, k, budget, r = [(6, 5, 800, 200, 3, 30, 1), (8, 7, 5000, 1000, 8, 64, 2),
+                                (4, 16, 600, 0, 2, 40, 0)][case]
+    x = W.make_tree_build_inputs(f"rs{case}", 200 + case, B=B, S=S, V=V, H=H, k=k, budget=budget)
+    rng = np.random.default_rng(case)
+    alen = rng.integers(0, S + 2, B).astype(np.int32)         # 0 .. S+1, every window kind
+    alen[0], alen[-1] = 1, S + 1
+    bonus = rng.integers(0, V, B).astype(np.int32)
+    if H:
+        bonus[1::2] = x.hot_vocab[rng.integers(0, H, len(bonus[1::2]))]
+    compare_resample(oracle_mod, T, x, bonus, alen, r, f"resample{case}")
+
+
+def test_resample_narrative(oracle_mod):
+    """The re-sampling narrative of §5.3 (golden fixture) on the GPU."""
+    T = U.require_gpu()
+    from tests.test_oracle_tree_build import resample_narrative
+    g, ids, logits, table, hot = resample_narrative()
+    V = len(g["vocab"])
+    x = W.TreeBuildInputs("rs-narrative", 1, logits.shape[1], V, V, g["k"], 16, logits,
+                          np.array([0], np.int32), table, hot, np.arange(V, dtype=np.int32))
+    got = compare_resample(oracle_mod, T, x, np.array([ids[g["bonus"]]], np.int32),
+                           np.array([g["accept_len"]], np.int32), g["r"], "rs-narrative")
+    names = [g["vocab"][t] for t in got[1][0][:3]]
+    assert names == ["quantization", "accuracy", "method"]
+
+
+def test_speculative_iteration_chain(oracle_mod):
+    """One speculative iteration end to end on the GPU, each stage checked
+    against the oracle: build the draft trees, verify them (greedy accept over
+    synthetic target logits with some drafts made acceptable), re-sample from
+    the bonus tokens and accepted lengths."""
+    T = U.require_gpu()
+    x = W.make_tree_build_inputs("chain", 77, B=6, S=5, V=2000, H=400, k=3, budget=24)
+    par, tok, jnt, nn = run_gpu(T, x)
+    want = oracle_mod.tree_build(x.logits, x.root, x.table, x.hot_vocab, x.k, x.budget)
+    np.testing.assert_array_equal(tok, want[1])
+    rng = np.random.default_rng(3)
+    tgt = rng.standard_normal((x.B, x.budget, x.V)).astype(np.float32)
+    for b in range(x.B):                                   # let the target agree on a path
+        depth = int(rng.integers(0, 4))
+        i = 0
+        for _ in range(depth):
+            kids = [c for c in range(1, nn[b]) if par[b, c] == i]
+            if not kids:
+                break
+            c = kids[int(rng.integers(0, len(kids)))]
+            tgt[b, i, tok[b, c]] += 50.0
+            i = c
+    a, alen, aidx, bonus = T.tree_argmax_accept(U.dev(tgt), U.dev(tok), U.dev(par),
+                                                num_nodes=U.dev(nn))
+    torch.cuda.synchronize()
+    alen, bonus = alen.cpu().numpy(), bonus.cpu().numpy()
+    rl, ri, rb = oracle_mod.accept(tok, par, oracle_mod.argmax(tgt), num_nodes=nn)
+    np.testing.assert_array_equal(alen, rl)
+    np.testing.assert_array_equal(bonus, rb)
+    print(f"accept_len {alen.tolist()}", flush=True)
+    compare_resample(oracle_mod, T, x, bonus, alen, 1, "chain-resample")
