@@ -231,11 +231,16 @@ def cpu_baseline(w, sample_b: int, min_seconds: float = 10.0):
                       f"(fp64 C, OpenMP), {dt:.2f} s"}
 
 
-def tree_build_bytes(x) -> int:
-    """Bytes the tree builder must move per call: every step's logits once,
-    the hot map once, one table row per expanded node, the outputs."""
-    expanded = x.B * (1 + (x.S - 1) * x.k)           # nodes whose children are drawn
-    return (x.B * x.S * x.V * 4 + (x.V * 4 + x.H * 4 if x.H else 0) + expanded * x.H * 2
+def tree_build_bytes(x, accept_len=None, r_min: int = 0) -> int:
+    """Bytes the tree builder must move per call: the logits rows it uses once,
+    the hot map once, one table row per expanded node, the outputs. With
+    accept_len (re-sampling) only the remaining rows of each sequence count."""
+    steps = np.full(x.B, x.S) if accept_len is None else np.maximum(x.S - accept_len, 0)
+    if accept_len is not None:
+        steps = np.where(steps > r_min, steps, 0)
+    rows = int(steps.sum())
+    expanded = int(sum(1 + (s - 1) * x.k for s in steps if s > 0))
+    return (rows * x.V * 4 + (x.V * 4 + x.H * 4 if x.H else 0) + expanded * x.H * 2
             + x.B * x.budget * 12 + x.B * 8)
 
 
@@ -244,6 +249,8 @@ def run_tree_build(args, T, torch):
     pruning) on one batch per step; value = draft trees per second."""
     from paper_2602_21224_amd import workloads as W
     x = W.tree_build_preset(args.workload)
+    resample = args.workload.startswith("rs_")
+    r_min = 1
     dev = torch.device("cuda:0")
     print(f"# workload {args.workload}: B={x.B} S={x.S} V={x.V} H={x.H} k={x.k} "
           f"budget={x.budget}", file=sys.stderr, flush=True)
@@ -252,6 +259,9 @@ def run_tree_build(args, T, torch):
     hot_vocab = up(x.hot_vocab) if x.H else None
     hot_index = up(x.hot_index) if x.H else None
     copies = [dict(logits=up(x.logits), root=up(x.root))]
+    if resample:
+        bonus, alen = W.resample_inputs(x, 7)
+        copies[0].update(bonus=up(bonus), alen=up(alen))
     copies += [{k: v.clone() for k, v in copies[0].items()} for _ in range(args.copies - 1)]
     ws = torch.empty(T.tree_build_workspace_size(x.B, x.S, x.V, x.H, x.k), dtype=torch.uint8,
                      device=dev)
@@ -265,9 +275,14 @@ def run_tree_build(args, T, torch):
     def step(i, ev=None):
         c, o = copies[i % len(copies)], outs[i % len(copies)]
         if ev: tev.record(ev[0], stream)
-        T.tree_build(c["logits"], c["root"], table, hot_vocab, hot_index, k=x.k, budget=x.budget,
-                     parent=o["parent"], token=o["token"], joint=o["joint"], num_nodes=o["nn"],
-                     workspace=ws)
+        if resample:
+            T.tree_resample(c["logits"], c["bonus"], c["alen"], table, hot_vocab, hot_index,
+                            k=x.k, r=r_min, budget=x.budget, parent=o["parent"],
+                            token=o["token"], joint=o["joint"], num_nodes=o["nn"], workspace=ws)
+        else:
+            T.tree_build(c["logits"], c["root"], table, hot_vocab, hot_index, k=x.k,
+                         budget=x.budget, parent=o["parent"], token=o["token"], joint=o["joint"],
+                         num_nodes=o["nn"], workspace=ws)
         if ev: tev.record(ev[1], stream)
 
     for i in range(args.warmup):
@@ -287,7 +302,7 @@ def run_tree_build(args, T, torch):
     for e in sampled:
         for q in e:
             tev.destroy(q)
-    nbytes = tree_build_bytes(x)
+    nbytes = tree_build_bytes(x, alen if resample else None, r_min)
     ach = nbytes / t_call.mean() / 1e9
     cpu = None
     if args.cpu_sample != 0:
@@ -295,7 +310,12 @@ def run_tree_build(args, T, torch):
         nb = x.B if args.cpu_sample < 0 else min(args.cpu_sample, x.B)
         reps, c0 = 0, time.perf_counter()
         while True:
-            oracle.tree_build(x.logits[:nb], x.root[:nb], x.table, x.hot_vocab, x.k, x.budget)
+            if resample:
+                oracle.resample(x.logits[:nb], bonus[:nb], alen[:nb], x.table, x.hot_vocab, x.k,
+                                r_min, x.budget)
+            else:
+                oracle.tree_build(x.logits[:nb], x.root[:nb], x.table, x.hot_vocab, x.k,
+                                  x.budget)
             reps += 1
             dt = time.perf_counter() - c0
             if dt >= 10.0 or reps >= 50:
@@ -305,7 +325,8 @@ def run_tree_build(args, T, torch):
                "sample": f"{nb} of {x.B} sequences of the same workload, {reps} passes "
                          f"(numpy, one thread), {dt:.2f} s"}
     line = {
-        "metric": "draft trees/sec (token-info sampling + budget pruning), 1 GPU",
+        "metric": ("re-sampled draft trees/sec (Alg. 2 + budget pruning), 1 GPU" if resample else
+                   "draft trees/sec (token-info sampling + budget pruning), 1 GPU"),
         "value": round(x.B / (wall / args.steps), 1), "unit": "draft trees/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,

@@ -450,8 +450,9 @@ def make_tree_build_inputs(name: str, seed: int, *, B: int, S: int, V: int, H: i
 
 
 TREE_BUILD_PRESETS = {
-    # name: (seed, B, S, V, H, k, budget)
+    # name: (seed, B, S, V, H, k, budget); "rs_" presets re-sample (Alg. 2)
     "tb_tiny": (40, 2, 3, 300, 60, 3, 16),
+    "rs_llama8b_bs16": (43, 16, 7, 128256, 32768, 8, 64),
     "tb_llama2_bs16": (41, 16, 7, 32000, 32000, 8, 64),
     "tb_llama8b_bs16": (42, 16, 7, 128256, 32768, 8, 64),
 }
@@ -462,7 +463,22 @@ TREE_BUILD_DOC = {
                       "§6.1), k 8, budget 64",
     "tb_llama8b_bs16": "batch 16, 7 steps, vocab 128256 with the 32768 hot tokens of §6.1, "
                        "k 8, budget 64",
+    "rs_llama8b_bs16": "re-sampling after verification at the tb_llama8b_bs16 shapes: accept "
+                       "lengths U{1..4} (seeded), bonus tokens hot w.p. 0.75, threshold r = 1",
 }
+
+
+def resample_inputs(x: TreeBuildInputs, seed: int):
+    """Verification outcome that drives re-sampling: accept lengths U{1..4}
+    (the root plus up to three accepted drafts) and bonus tokens, hot with
+    probability 0.75."""
+    rng = np.random.default_rng(seed)
+    alen = rng.integers(1, 5, x.B).astype(np.int32)
+    bonus = rng.integers(0, x.V, x.B).astype(np.int32)
+    if x.H > 0:
+        hot = rng.random(x.B) < 0.75
+        bonus[hot] = x.hot_vocab[rng.integers(0, x.H, int(hot.sum()))]
+    return bonus, alen
 
 
 def tree_build_preset(name: str) -> TreeBuildInputs:
