@@ -202,3 +202,4 @@ def kv_compact(k_tree, v_tree, k_cache, v_cache, page_table, kv_len, accept_idx,
 
 
 from .tree_build import resample, tree_build  # noqa: E402  (Alg. 1, Alg. 2, pruning; numpy)
+from .lm_head import lm_head_argmax, lm_head_logits  # noqa: E402  (LM head + argmax; numpy)
