@@ -142,6 +142,7 @@ CALL_KERNELS = {
     "tree_argmax_accept": ("argmax_segments_kernel", "accept_kernel"),
     "kv_compact_accepted": ("kv_compact_kernel",),
     "tree_build": ("tb_rows_kernel", "tb_expand_kernel", "tb_select_kernel", "tb_prune_kernel"),
+    "tree_lm_head_argmax_accept": ("lm_keys_clear_kernel", "lm_head_argmax_kernel", "accept_kernel"),
 }
 
 
@@ -347,6 +348,111 @@ def run_tree_build(args, T, torch):
     print(json.dumps(line), flush=True)
 
 
+def run_lm_head(args, T, torch):
+    """The LM head fused with greedy verification (hidden states x head
+    weight, per-node argmax, acceptance) on one batch per step; value =
+    verified tree-tokens per second. The roofline is the matrix cores'
+    (2 R V d flops per call against the dense bf16 peak)."""
+    from paper_2602_21224_amd import workloads as W
+    x = W.lm_head_preset(args.workload)
+    dev = torch.device("cuda:0")
+    R = x.B * x.N
+    print(f"# workload {args.workload}: B={x.B} N={x.N} V={x.V} d={x.d}", file=sys.stderr,
+          flush=True)
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    w_head = up(x.w_head.view(np.int16)).view(torch.bfloat16)
+    copies = [dict(hidden=up(x.hidden.view(np.int16)).view(torch.bfloat16), draft=up(x.draft),
+                   parent=up(x.parent))]
+    copies += [{k: v.clone() for k, v in copies[0].items()} for _ in range(args.copies - 1)]
+    ws = torch.empty(T.lm_head_workspace_size(x.B, x.N, x.V, x.d), dtype=torch.uint8, device=dev)
+    mk = lambda *shape: torch.empty(shape, dtype=torch.int32, device=dev)
+    outs = [dict(amax=mk(x.B, x.N), alen=mk(x.B), aidx=mk(x.B, x.N), bonus=mk(x.B))
+            for _ in copies]
+    stream = torch.cuda.current_stream()
+    tev = TimingEvents()
+
+    def step(i, ev=None):
+        c, o = copies[i % len(copies)], outs[i % len(copies)]
+        if ev: tev.record(ev[0], stream)
+        T.tree_lm_head_argmax_accept(c["hidden"], w_head, c["draft"], c["parent"],
+                                     argmax_out=o["amax"], accept_len=o["alen"],
+                                     accept_idx=o["aidx"], bonus_token=o["bonus"], workspace=ws)
+        if ev: tev.record(ev[1], stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ev_every = max(1, min(4, args.steps // 8))
+    evs = [[tev.create() for _ in range(2)] if i % ev_every == 0 else None
+           for i in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    sampled = [e for e in evs if e is not None]
+    t_call = np.array([tev.seconds(e[0], e[1]) for e in sampled])
+    # Context: the library GEMM of the same product (bf16 logits written to HBM,
+    # no argmax), timed the same way.
+    hid2 = copies[0]["hidden"].reshape(R, x.d)
+    for _ in range(5):
+        torch.nn.functional.linear(hid2, w_head)
+    torch.cuda.synchronize()
+    t_lib = []
+    for e in sampled[:8]:
+        tev.record(e[0], stream)
+        torch.nn.functional.linear(hid2, w_head)
+        tev.record(e[1], stream)
+        torch.cuda.synchronize()
+        t_lib.append(tev.seconds(e[0], e[1]))
+    for e in sampled:
+        for q in e:
+            tev.destroy(q)
+    alen = outs[(args.warmup + args.steps - 1) % len(copies)]["alen"].cpu().numpy()
+    flop = 2.0 * R * x.V * x.d
+    tflops = flop / t_call.mean() / 1e12
+    cpu = None
+    if args.cpu_sample != 0:
+        import oracle
+        nr = 16
+        reps, c0 = 0, time.perf_counter()
+        while True:
+            oracle.lm_head_argmax(x.hidden.reshape(R, x.d)[:nr], x.w_head)
+            reps += 1
+            dt = time.perf_counter() - c0
+            if dt >= 10.0:
+                break
+        cpu = {"value": round(reps * nr / dt, 2), "unit": "verified tree-tokens/s",
+               "cores": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)),
+               "kind": "oracle",
+               "sample": f"LM-head argmax of the first {nr} of {R} node rows over the whole "
+                         f"vocabulary, {reps} passes (numpy fp64 matmul), {dt:.2f} s"}
+    line = {
+        "metric": "verified tree-tokens/sec (LM head fused with argmax + accept), 8B-shaped, "
+                  "1 GPU",
+        "value": round(R / (wall / args.steps), 1), "unit": "verified tree-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "batch": x.B, "tree_nodes": x.N, "vocab": x.V,
+                   "hidden": x.d, "input_copies_rotated": len(copies)},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "tree_lm_head_argmax_accept",
+                     "avg_us": round(t_call.mean() * 1e6, 2), "algorithmic_flop": flop,
+                     "launches_per_call": 3},
+        "call_us_p50": round(float(np.median(t_call)) * 1e6, 2),
+        "library_gemm_bf16_out_us": round(float(np.median(t_lib)) * 1e6, 2) if t_lib else None,
+        "accept_len_hist": np.bincount(alen, minlength=1).tolist(),
+        "timed_steps_with_events": len(sampled),
+        "cpu_baseline": cpu,
+        "source_digest": source_digest(),
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -392,6 +498,9 @@ def main():
     T.load()
     if args.workload in W.TREE_BUILD_PRESETS:
         run_tree_build(args, T, torch)
+        return
+    if args.workload in W.LM_HEAD_PRESETS:
+        run_lm_head(args, T, torch)
         return
     w = W.preset(args.workload)
     print(f"# workload {args.workload}: B={w.B} N={w.N} Hq={w.Hq} Hkv={w.Hkv} D={w.D} "

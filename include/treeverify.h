@@ -73,7 +73,7 @@ extern "C" {
 #define TV_API
 #endif
 
-#define TV_ABI_VERSION 3
+#define TV_ABI_VERSION 4
 
 enum tv_status {
     TV_OK = 0,
@@ -305,6 +305,46 @@ TV_API int tree_build(const float *logits, const int32_t *root_token, const uint
                       int H, int k, int budget, int32_t *parent, int32_t *token, float *joint,
                       int32_t *num_nodes, void *workspace, size_t workspace_bytes,
                       hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * tree_lm_head_argmax_accept  (LM head fused with greedy verification)
+ *
+ * The logits tree_argmax_accept consumes are the target model's LM head
+ * applied to every node's final hidden state, all nodes in one matrix
+ * product (the paper computes the draft's logits of many positions the same
+ * way, §4.2). This call takes the hidden states and the head weight instead
+ * and never stores logits:
+ *   logit[r, v]  = sum_i hidden[r, i] * w_head[v, i]    (bf16 products, fp32
+ *                                                       accumulation on the
+ *                                                       matrix cores)
+ *   argmax_out[b, i] = lowest v maximising logit[b * N + i, v] as computed
+ *                      (same ordering as tree_argmax_accept: -0 == +0, NaN
+ *                      counts as the maximum)
+ * and then exactly the acceptance of tree_argmax_accept (accept_len,
+ * accept_idx, bonus_token, num_nodes handling). Where two logits of a row
+ * lie within the fp32 accumulation error of each other, which of them wins
+ * depends on the accumulation order; the result is then one of them.
+ *
+ *   hidden       [B, N, d]   bf16, 16-byte aligned
+ *   w_head       [V, d]      bf16, 16-byte aligned (row v = token v's weights)
+ *   draft_tokens, parent [B, N], num_nodes [B] (or NULL), argmax_out [B, N],
+ *   accept_len [B], accept_idx [B, N], bonus_token [B]: as tree_argmax_accept.
+ *                Padding rows are multiplied with the rest (fixed tile shape)
+ *                but take no part in any result.
+ *   workspace    >= tv_lm_head_workspace_size(B, N, V, d) bytes of device
+ *                memory, 8-byte aligned; contents on entry do not matter.
+ * Supported: 0 <= B <= 65535, 1 <= N <= 256, 1 <= V < 2^31, d a multiple of
+ * 32 (>= 32), and at most 2^31 - 1 workgroups (V/256 x B N/256, rounded up).
+ * ------------------------------------------------------------------------ */
+TV_API size_t tv_lm_head_workspace_size(int B, int N, int V, int d);
+
+TV_API int tree_lm_head_argmax_accept(const uint16_t *hidden, const uint16_t *w_head,
+                                      const int32_t *draft_tokens, const int32_t *parent,
+                                      const int32_t *num_nodes, int B, int N, int V, int d,
+                                      int32_t *argmax_out, int32_t *accept_len,
+                                      int32_t *accept_idx, int32_t *bonus_token,
+                                      void *workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
 
 #ifdef __cplusplus
 }

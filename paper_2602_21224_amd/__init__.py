@@ -6,7 +6,8 @@ library.
 """
 
 __all__ = ["tree_verify_attention", "tree_argmax_accept", "kv_compact_accepted",
-           "tv_validate_inputs", "tree_build", "tree_resample", "attention_workspace_size",
+           "tv_validate_inputs", "tree_build", "tree_resample", "tree_lm_head_argmax_accept",
+           "attention_workspace_size", "lm_head_workspace_size",
            "argmax_workspace_size", "tree_build_workspace_size", "abi_version", "load"]
 
 

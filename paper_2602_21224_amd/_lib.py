@@ -56,6 +56,10 @@ def load():
     lib.tree_build.restype = i
     lib.tree_resample.argtypes = [p] * 6 + [i] * 7 + [p] * 5 + [sz, p]
     lib.tree_resample.restype = i
+    lib.tv_lm_head_workspace_size.argtypes = [i] * 4
+    lib.tv_lm_head_workspace_size.restype = sz
+    lib.tree_lm_head_argmax_accept.argtypes = [p] * 5 + [i] * 4 + [p] * 5 + [sz, p]
+    lib.tree_lm_head_argmax_accept.restype = i
     _lib = lib
     return lib
 
@@ -173,6 +177,46 @@ def tree_argmax_accept(logits, draft_tokens, parent, *, num_nodes=None, argmax_o
         _ptr(accept_len), _ptr(accept_idx), _ptr(bonus_token), _ptr(workspace),
         workspace.numel(), _stream(stream))
     _check(st, "tree_argmax_accept")
+    return argmax_out, accept_len, accept_idx, bonus_token
+
+
+def lm_head_workspace_size(B, N, V, d) -> int:
+    return int(load().tv_lm_head_workspace_size(B, N, V, d))
+
+
+def tree_lm_head_argmax_accept(hidden, w_head, draft_tokens, parent, *, num_nodes=None,
+                               argmax_out=None, accept_len=None, accept_idx=None,
+                               bonus_token=None, workspace=None, stream=None):
+    """LM head fused with greedy verification: hidden [B,N,d] bf16 times
+    w_head [V,d] bf16, per-node argmax of the product (never stored), then the
+    acceptance of tree_argmax_accept.
+    Returns (argmax [B,N], accept_len [B], accept_idx [B,N], bonus [B]) int32."""
+    B, N, d = hidden.shape
+    V = w_head.shape[0]
+    dev = hidden.device
+    _want(hidden, "hidden", _BF16)
+    _want(w_head, "w_head", _BF16, (V, d))
+    _want(draft_tokens, "draft_tokens", (torch.int32,), (B, N))
+    _want(parent, "parent", (torch.int32,), (B, N))
+    if num_nodes is not None:
+        _want(num_nodes, "num_nodes", (torch.int32,), (B,))
+    mk = lambda shape: torch.empty(shape, dtype=torch.int32, device=dev)
+    argmax_out = mk((B, N)) if argmax_out is None else argmax_out
+    accept_len = mk((B,)) if accept_len is None else accept_len
+    accept_idx = mk((B, N)) if accept_idx is None else accept_idx
+    bonus_token = mk((B,)) if bonus_token is None else bonus_token
+    for t, n, s in ((argmax_out, "argmax_out", (B, N)), (accept_len, "accept_len", (B,)),
+                    (accept_idx, "accept_idx", (B, N)), (bonus_token, "bonus_token", (B,))):
+        _want(t, n, (torch.int32,), s)
+    need = lm_head_workspace_size(B, N, V, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    _want(workspace, "workspace", (torch.uint8,))
+    st = load().tree_lm_head_argmax_accept(
+        _ptr(hidden), _ptr(w_head), _ptr(draft_tokens), _ptr(parent), _ptr(num_nodes), B, N, V,
+        d, _ptr(argmax_out), _ptr(accept_len), _ptr(accept_idx), _ptr(bonus_token),
+        _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "tree_lm_head_argmax_accept")
     return argmax_out, accept_len, accept_idx, bonus_token
 
 

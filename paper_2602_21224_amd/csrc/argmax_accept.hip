@@ -180,8 +180,17 @@ hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const
                                        dim3(kArgmaxThreads), s, logits, num_nodes, N, V, segs,
                                        seg_len, ws);
     if (e != hipSuccess) return e;
-    return launch_kernel(accept_kernel, dim3(B), dim3(kAcceptThreads), s, ws, segs, draft, parent,
-                         num_nodes, N, argmax_out, accept_len, accept_idx, bonus);
+    return launch_accept(ws, segs, draft, parent, num_nodes, B, N, argmax_out, accept_len,
+                         accept_idx, bonus, s);
+}
+
+hipError_t launch_accept(const unsigned long long *keys, int segs, const int32_t *draft,
+                         const int32_t *parent, const int32_t *num_nodes, int B, int N,
+                         int32_t *argmax_out, int32_t *accept_len, int32_t *accept_idx,
+                         int32_t *bonus, hipStream_t s) {
+    if (B == 0) return hipSuccess;
+    return launch_kernel(accept_kernel, dim3(B), dim3(kAcceptThreads), s, keys, segs, draft,
+                         parent, num_nodes, N, argmax_out, accept_len, accept_idx, bonus);
 }
 
 }  // namespace tv

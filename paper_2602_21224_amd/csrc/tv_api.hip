@@ -317,4 +317,38 @@ int tree_resample(const float *logits, const int32_t *bonus_token, const int32_t
     return e == hipSuccess ? TV_OK : TV_ERR_HIP;
 }
 
+static bool lm_head_shape_ok(int B, int N, int V, int d) {
+    if (B < 0 || B > 65535 || N < 1 || N > tv::kMaxNodes || V < 1 || d < 32 || d % 32 != 0)
+        return false;
+    const long long rblocks = ((long long)B * N + 255) / 256;
+    const long long groups = ((long long)tv::lm_head_vocab_tiles(V) + 7) / 8 * 8 * rblocks;
+    return groups <= 0x7FFFFFFFll;
+}
+
+size_t tv_lm_head_workspace_size(int B, int N, int V, int d) {
+    if (!lm_head_shape_ok(B, N, V, d)) return 0;
+    return round_up((size_t)B * N * sizeof(unsigned long long), 256) + 256;
+}
+
+int tree_lm_head_argmax_accept(const uint16_t *hidden, const uint16_t *w_head,
+                               const int32_t *draft_tokens, const int32_t *parent,
+                               const int32_t *num_nodes, int B, int N, int V, int d,
+                               int32_t *argmax_out, int32_t *accept_len, int32_t *accept_idx,
+                               int32_t *bonus_token, void *workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
+    if (!lm_head_shape_ok(B, N, V, d)) return TV_ERR_SHAPE;
+    if (B == 0) return TV_OK;
+    if (!hidden || !w_head || !draft_tokens || !parent || !argmax_out || !accept_len ||
+        !accept_idx || !bonus_token || !workspace)
+        return TV_ERR_NULL;
+    if (!aligned16(hidden) || !aligned16(w_head) || (reinterpret_cast<uintptr_t>(workspace) & 7u))
+        return TV_ERR_ALIGN;
+    if (workspace_bytes < tv_lm_head_workspace_size(B, N, V, d)) return TV_ERR_WORKSPACE;
+    if (!device_ok()) return TV_ERR_DEVICE;
+    const hipError_t e = tv::launch_lm_head_argmax_accept(
+        hidden, w_head, draft_tokens, parent, num_nodes, B, N, V, d, argmax_out, accept_len,
+        accept_idx, bonus_token, static_cast<unsigned long long *>(workspace), stream);
+    return e == hipSuccess ? TV_OK : TV_ERR_HIP;
+}
+
 }  // extern "C"

@@ -111,6 +111,18 @@ hipError_t launch_argmax_accept(const float *logits, const int32_t *draft, const
                                 int seg_len, int32_t *argmax_out,
                                 int32_t *accept_len, int32_t *accept_idx, int32_t *bonus,
                                 unsigned long long *ws, hipStream_t s);
+// Greedy acceptance over per-node argmax keys: keys[(b * N + i) * segs + s].
+hipError_t launch_accept(const unsigned long long *keys, int segs, const int32_t *draft,
+                         const int32_t *parent, const int32_t *num_nodes, int B, int N,
+                         int32_t *argmax_out, int32_t *accept_len, int32_t *accept_idx,
+                         int32_t *bonus, hipStream_t s);
+int lm_head_vocab_tiles(int V);
+hipError_t launch_lm_head_argmax_accept(const uint16_t *hidden, const uint16_t *w,
+                                        const int32_t *draft, const int32_t *parent,
+                                        const int32_t *num_nodes, int B, int N, int V, int d,
+                                        int32_t *argmax_out, int32_t *accept_len,
+                                        int32_t *accept_idx, int32_t *bonus,
+                                        unsigned long long *keys, hipStream_t s);
 hipError_t launch_kv_compact(const uint16_t *k_tree, const uint16_t *v_tree, uint16_t *k_cache,
                              uint16_t *v_cache, const int32_t *page_table, const int32_t *kv_len,
                              const int32_t *accept_idx, const int32_t *accept_len, int B, int N,

@@ -484,3 +484,94 @@ def resample_inputs(x: TreeBuildInputs, seed: int):
 def tree_build_preset(name: str) -> TreeBuildInputs:
     seed, B, S, V, H, k, budget = TREE_BUILD_PRESETS[name]
     return make_tree_build_inputs(name, seed, B=B, S=S, V=V, H=H, k=k, budget=budget)
+
+
+# ---------------------------------------------------------------------------
+# Inputs of the LM head fused with greedy verification: every tree node's final
+# hidden state and the target model's LM-head weight, plus the draft trees.
+@dataclass
+class LmHeadInputs:
+    name: str
+    B: int
+    N: int
+    V: int
+    d: int
+    hidden: np.ndarray     # [B, N, d] uint16 (bf16 bits)
+    w_head: np.ndarray     # [V, d] uint16 (bf16 bits), row v = token v
+    parent: np.ndarray     # [B, N] int32
+    draft: np.ndarray      # [B, N] int32
+    num_nodes: np.ndarray | None   # [B] int32, or None (N nodes each)
+    planted: np.ndarray    # [B, N] int32: token whose logit was raised, -1 if none
+
+
+def _uniform_bf16(rng: np.random.Generator, shape, std: float, rows_per_chunk: int = 8192):
+    """Uniform(-sqrt(3) std, sqrt(3) std) cut to bf16 by truncation, drawn in
+    row chunks (the full 8B-shaped head is 128256 x 4096)."""
+    out = np.empty(shape, dtype=np.uint16)
+    a = np.float32(2.0 * 3.0 ** 0.5 * std)
+    for r0 in range(0, shape[0], rows_per_chunk):
+        r1 = min(shape[0], r0 + rows_per_chunk)
+        x = (rng.random((r1 - r0,) + tuple(shape[1:]), dtype=np.float32) - np.float32(0.5)) * a
+        out[r0:r1] = (x.view(np.uint32) >> 16).astype(np.uint16)
+    return out
+
+
+def make_lm_head_inputs(name: str, seed: int, *, B: int, N: int, V: int, d: int,
+                        w_std: float = 0.02, plant_prob: float = 0.6, plant_gain: float = 6.0,
+                        depth_lt: int = 8, num_nodes=None) -> LmHeadInputs:
+    """Seeded synthetic inputs. Hidden states are N(0, 1) (a normalised final
+    hidden state), the head is uniform with standard deviation w_std, so the
+    logits spread with standard deviation about sqrt(d) w_std. Trees are
+    depth-capped random trees (as in the llama8b_bs16 verification preset);
+    for each node with children, with probability plant_prob the hidden state
+    is moved along the head row of one random child's draft token so that this
+    token's logit rises by about plant_gain (the child becomes acceptable, as
+    a good draft would be). `num_nodes` (optional [B]) makes the batch ragged;
+    padding rows keep random data."""
+    ss = np.random.SeedSequence(seed)
+    r_tree, r_tok, r_h, r_w, r_plant = (np.random.default_rng(s) for s in ss.spawn(5))
+    counts = (np.full(B, N, dtype=np.int32) if num_nodes is None
+              else np.asarray(num_nodes, dtype=np.int32))
+    parent = np.full((B, N), -1, dtype=np.int32)
+    draft = np.zeros((B, N), dtype=np.int32)
+    for b in range(B):
+        n = int(counts[b])
+        if n:
+            parent[b, :n] = tree_random_depth_capped(r_tree, n, depth_lt)
+            draft[b, :n] = draft_tokens(r_tok, parent[b, :n], V, True)
+    w_bits = _uniform_bf16(r_w, (V, d), w_std)
+    h = r_h.standard_normal((B, N, d), dtype=np.float32)
+    planted = np.full((B, N), -1, dtype=np.int32)
+    for b in range(B):
+        n = int(counts[b])
+        kids: dict[int, list] = {}
+        for i in range(n):
+            if parent[b, i] >= 0:
+                kids.setdefault(int(parent[b, i]), []).append(i)
+        for p in range(n):
+            ch = kids.get(p)
+            if ch and r_plant.random() < plant_prob:
+                t = int(draft[b, ch[int(r_plant.integers(0, len(ch)))]])
+                wt = bf16_bits_to_f32(w_bits[t]).astype(np.float64)
+                h[b, p] += np.float32(plant_gain / max(float(wt @ wt), 1e-30)) * wt.astype(np.float32)
+                planted[b, p] = t
+    return LmHeadInputs(name, B, N, V, d, f32_to_bf16_bits(h), w_bits, parent, draft,
+                        None if num_nodes is None else counts, planted)
+
+
+LM_HEAD_PRESETS = {
+    # name: (seed, B, N, V, d)
+    "lm_tiny": (50, 2, 16, 1000, 256),
+    "lm_llama8b_bs16": (51, 16, 64, 128256, 4096),
+}
+
+LM_HEAD_DOC = {
+    "lm_tiny": "batch 2, 16-node trees, vocab 1000, hidden size 256",
+    "lm_llama8b_bs16": "batch 16, 64-node random trees (depth <= 8), vocab 128256, hidden "
+                       "size 4096 (Llama-3-8B's LM head), planted acceptable drafts w.p. 0.6",
+}
+
+
+def lm_head_preset(name: str) -> LmHeadInputs:
+    seed, B, N, V, d = LM_HEAD_PRESETS[name]
+    return make_lm_head_inputs(name, seed, B=B, N=N, V=V, d=d)

@@ -47,7 +47,7 @@ def test_only_declared_symbols_are_exported():
 
 
 def test_status_strings(lib):
-    assert lib.tv_abi_version() == 3
+    assert lib.tv_abi_version() == 4
     for code in range(0, -7, -1):
         assert lib.tv_status_string(code)
     assert lib.tv_status_string(-99) == b"unknown status"
@@ -150,3 +150,23 @@ def test_tree_resample_argument_checks(lib):
     assert rs(r=-1) == -2 and rs(S=17) == -2 and rs(budget=0) == -2
     assert rs(ws_bytes=lib.tv_tree_build_workspace_size(2, 4, 1000, 100, 4) - 1) == -4
 
+
+
+def test_lm_head_argument_checks(lib):
+    def lm(**kw):
+        a = dict(hidden=FAKE, w=FAKE, draft=FAKE, parent=FAKE, num_nodes=NULL, B=2, N=64,
+                 V=1000, d=256, amax=FAKE, alen=FAKE, aidx=FAKE, bonus=FAKE, ws=FAKE,
+                 ws_bytes=1 << 40)
+        a.update(kw)
+        return lib.tree_lm_head_argmax_accept(*a.values(), STREAM)
+    assert lm(B=0) == 0
+    assert lm(hidden=NULL) == -1 and lm(w=NULL) == -1 and lm(bonus=NULL) == -1
+    assert lm(ws=NULL) == -1
+    assert lm(d=0) == -2 and lm(d=48) == -2 and lm(d=16) == -2          # d: multiple of 32
+    assert lm(V=0) == -2 and lm(N=257) == -2 and lm(B=65536) == -2
+    assert lm(B=65535, N=256, V=(1 << 31) - 1) == -2                    # grid above 2^31 - 1
+    assert lm(hidden=ctypes.c_void_p(0x10008)) == -3 and lm(w=ctypes.c_void_p(0x10008)) == -3
+    assert lm(ws=ctypes.c_void_p(0x10004)) == -3
+    need = lib.tv_lm_head_workspace_size(2, 64, 1000, 256)
+    assert need >= 2 * 64 * 8 and lm(ws_bytes=need - 1) == -4
+    assert lib.tv_lm_head_workspace_size(2, 64, 1000, 40) == 0
