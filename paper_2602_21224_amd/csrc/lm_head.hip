@@ -12,18 +12,21 @@
 // lower id on ties), so the [rows, V] fp32 logits never exist in memory.
 //
 //   * Workgroup tile: 256 vocabulary entries (MFMA M) x 256 hidden rows
-//     (MFMA N). Four waves in a 2 x 2 arrangement, each accumulating a
-//     128 x 128 block in 16 fp32 v_mfma_f32_32x32x16_bf16 accumulators.
+//     (MFMA N), the largest whose fp32 accumulators fit a CU's registers.
+//     Eight waves (two per SIMD, so one wave's waits are covered by the
+//     other's matrix work) in a 2 x 4 arrangement, each accumulating a
+//     128 x 64 block in 8 v_mfma_f32_32x32x16_bf16 accumulators.
 //   * Both operands are K-contiguous (W is [V, d], hidden is [R, d]), so both
 //     stream into LDS the same way: global_load_lds_dwordx4 into a 4-stage
-//     ring of 32-deep K slices, issued three slices ahead. The four 16-byte
-//     chunks of each 64-byte row slice are XOR-swizzled by bits 2-3 of the
-//     row, so the operand reads (16 rows at one chunk per LDS pass) are free
-//     of bank conflicts.
-//   * Operand reads for the next K step are issued before the current step's
-//     16 MFMAs, and the ring hand-off (s_waitcnt vmcnt + s_barrier) sits
-//     between the two K steps of a slice, so the matrix pipe sees no wait for
-//     LDS data in steady state.
+//     ring of 32-deep K slices. The four 16-byte chunks of each 64-byte row
+//     slice are XOR-swizzled by bits 2-3 of the row, so the operand reads
+//     (16 rows at one chunk per LDS pass) are free of bank conflicts.
+//   * The reads of the next K step's operands and the loads of the slice
+//     four ahead are interleaved one by one with the current step's MFMAs
+//     (pinned by sched_barrier), and the ring hand-off (s_waitcnt vmcnt +
+//     s_barrier) sits a few MFMAs into a slice's second K step, after this
+//     wave's last read of the slice whose stage is refilled next: three
+//     slices are in flight while one is computed.
 //   * Workgroup order: ids are dispatched round-robin over the 8 XCDs, so
 //     they are mapped such that the row blocks of one vocabulary tile run back
 //     to back on one XCD and share its L2 copy of that weight tile.
@@ -41,7 +44,8 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kLmThreads = 256;                        // 4 waves
+constexpr int kWaves = 8;                              // two per SIMD
+constexpr int kLmThreads = kWaves * kWave;
 constexpr int kTileM = 256;                            // vocabulary entries per workgroup
 constexpr int kTileN = 256;                            // hidden rows per workgroup
 constexpr int kBK = 32;                                // K depth of one ring stage
@@ -50,13 +54,16 @@ constexpr int kSliceRow = kBK * 2;                     // bytes of one row's K s
 constexpr int kOperandBytes = kTileM * kSliceRow;      // 16 KB per operand per stage
 constexpr int kStageBytes = 2 * kOperandBytes;         // W slice, then hidden slice
 constexpr int kLoads = kOperandBytes / (kLmThreads * 16);   // 16-byte loads per operand per thread
-constexpr int kWaveM = 128, kWaveN = 128;              // per-wave block
+constexpr int kWaveM = 128;                            // per-wave block: 2 waves along M
+constexpr int kWaveN = kTileN / (kWaves / 2);
 constexpr int kFragM = kWaveM / 32, kFragN = kWaveN / 32;
+constexpr int kReads = kFragM + kFragN;                // fragment reads per K step
+constexpr int kSteps = kFragM * kFragN;                // MFMAs per K step
 static_assert(kTileM == kTileN, "both operands share one slice layout");
-static_assert(kLoads == 4, "one 1 KB block per load instruction and wave: 16 blocks per operand");
+static_assert(kLoads * kWaves == 16, "one 1 KB block per load instruction: 16 blocks per operand");
 
 __shared__ __attribute__((aligned(1024))) unsigned char g_lm_ring[kStages * kStageBytes];
-__shared__ unsigned long long g_lm_keys[2][kWaveN];
+__shared__ unsigned long long g_lm_keys[kWaves / 2][kWaveN];
 
 __device__ __forceinline__ unsigned lds_addr(const void *p) {
     return (unsigned)(size_t)(const LDS_AS void *)p;
@@ -95,7 +102,7 @@ __global__ void lm_keys_clear_kernel(unsigned long long *__restrict__ keys, int 
     if (i < R) keys[i] = 0ull;                  // below every real key
 }
 
-// grid: kNumXcd * ceil(vtiles / kNumXcd) * rblocks workgroups of 256 threads.
+// grid: kNumXcd * ceil(vtiles / kNumXcd) * rblocks workgroups of kLmThreads threads.
 __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
     const uint16_t *__restrict__ hidden, const uint16_t *__restrict__ w, int R, int V, int d,
     int vtiles, int rblocks, unsigned long long *__restrict__ keys) {
@@ -126,19 +133,6 @@ __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
         }
     }
     const int T = d / kBK;
-    auto issue = [&](int t) {
-        unsigned char *st = g_lm_ring + (t & (kStages - 1)) * kStageBytes;
-        const size_t koff = (size_t)t * kSliceRow;
-        #pragma unroll
-        for (int i = 0; i < kLoads; ++i)
-            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(asrc[i] + koff),
-                                             (LDS_AS void *)(st + (wave * kLoads + i) * 1024), 16, 0, 0);
-        #pragma unroll
-        for (int i = 0; i < kLoads; ++i)
-            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(bsrc[i] + koff),
-                                             (LDS_AS void *)(st + kOperandBytes + (wave * kLoads + i) * 1024),
-                                             16, 0, 0);
-    };
 
     // Operand fragments of v_mfma_f32_32x32x16_bf16: lane l reads row l % 32
     // of a 32-row block, K elements 8 (l / 32) .. +7 of the 16-deep step, i.e.
@@ -159,57 +153,120 @@ __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
             for (int e = 0; e < 16; ++e) acc[m][n][e] = 0.f;
     u32x4 fa[2][kFragM], fb[2][kFragN];
 
-    auto read = [&](int set, int stage, int s) {
-        const unsigned sb = ring + (unsigned)(stage * kStageBytes);
-        const unsigned aa = (sb + a_lane) ^ ((unsigned)s << 5);
-        const unsigned ba = (sb + b_lane) ^ ((unsigned)s << 5);
-        #pragma unroll
-        for (int m = 0; m < kFragM; ++m)
-            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(fa[set][m]) : "v"(aa), "i"(m * 32 * kSliceRow));
-        #pragma unroll
-        for (int n = 0; n < kFragN; ++n)
-            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(fb[set][n]) : "v"(ba), "i"(n * 32 * kSliceRow));
+    auto frag_addr = [&](int stage, int s, unsigned lane_off) {
+        return (ring + (unsigned)(stage * kStageBytes) + lane_off) ^ ((unsigned)s << 5);
     };
-    auto mma = [&](int set) {
+    // Read q (0..7) of a fragment set: A fragments 0..3, then B fragments 0..3.
+    auto read_q = [&](int set, unsigned aa, unsigned ba, int q) {
+        if (q < kFragM)
+            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(fa[set][q]) : "v"(aa), "i"(q * 32 * kSliceRow));
+        else
+            asm volatile("ds_read_b128 %0, %1 offset:%2"
+                         : "=v"(fb[set][q - kFragM]) : "v"(ba), "i"((q - kFragM) * 32 * kSliceRow));
+    };
+    auto ready = [&](int set) {             // after lds_wait_all: the set is in registers
         #pragma unroll
         for (int m = 0; m < kFragM; ++m) tie(fa[set][m]);
         #pragma unroll
         for (int n = 0; n < kFragN; ++n) tie(fb[set][n]);
-        #pragma unroll
-        for (int m = 0; m < kFragM; ++m)
-            #pragma unroll
-            for (int n = 0; n < kFragN; ++n)
-                acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8, fa[set][m]), __builtin_bit_cast(bf16x8, fb[set][n]),
-                    acc[m][n], 0, 0, 0);
+    };
+    auto mfma_q = [&](int set, int q) {
+        const int m = q / kFragN, n = q % kFragN;
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, fa[set][m]), __builtin_bit_cast(bf16x8, fb[set][n]),
+            acc[m][n], 0, 0, 0);
+    };
+    auto issue_load = [&](int t, int i) {     // load i (0 .. 2 kLoads - 1) of slice t
+        unsigned char *st = g_lm_ring + (t & (kStages - 1)) * kStageBytes;
+        const size_t koff = (size_t)t * kSliceRow;
+        if (i < kLoads)
+            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(asrc[i] + koff),
+                                             (LDS_AS void *)(st + (wave * kLoads + i) * 1024), 16, 0, 0);
+        else
+            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(bsrc[i - kLoads] + koff),
+                                             (LDS_AS void *)(st + kOperandBytes + (wave * kLoads + i - kLoads) * 1024),
+                                             16, 0, 0);
     };
 
-    // Slices 0..2 in flight; wait for slice 0 (later slices may stay pending).
-    issue(0);
-    if (T > 1) issue(1);
-    if (T > 2) issue(2);
-    if (T > 2) wait_vmcnt<4 * kLoads>();
+    // One K slice j. Step (j, 0) is in fragment set 0 (reads issued earlier).
+    // First half: its 16 MFMAs with the reads of step (j, 1) into set 1 between
+    // them. Second half: set 1's MFMAs; after the first four, the ring hand-off
+    // (slice j + 1 landed everywhere; every wave is done with slice j, whose
+    // stage slice j + 4 takes), then the loads of slice j + 4 and the reads of
+    // step (j + 1, 0) between the rest. sched_barrier pins the interleaving.
+    auto slice = [&](int j, bool more, bool load4, auto wait_next) {
+        constexpr int kPre = kSteps / 4;                 // MFMAs before the hand-off
+        constexpr int kOps = 2 * kLoads + kReads;        // loads, then reads, after it
+        constexpr int kPer = (kOps + kSteps - kPre - 1) / (kSteps - kPre);
+        lds_wait_all();
+        ready(0);
+        {
+            const unsigned aa = frag_addr(j & (kStages - 1), 1, a_lane);
+            const unsigned ba = frag_addr(j & (kStages - 1), 1, b_lane);
+            #pragma unroll
+            for (int q = 0; q < kSteps; ++q) {
+                mfma_q(0, q);
+                if (q < kReads) read_q(1, aa, ba, q);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        lds_wait_all();
+        ready(1);
+        #pragma unroll
+        for (int q = 0; q < kPre; ++q) {
+            mfma_q(1, q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (more) {
+            wait_next();
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const unsigned aa = frag_addr((j + 1) & (kStages - 1), 0, a_lane);
+        const unsigned ba = frag_addr((j + 1) & (kStages - 1), 0, b_lane);
+        #pragma unroll
+        for (int q = kPre; q < kSteps; ++q) {
+            mfma_q(1, q);
+            #pragma unroll
+            for (int u = 0; u < kPer; ++u) {
+                const int op = (q - kPre) * kPer + u;
+                if (op < 2 * kLoads) {
+                    if (load4) issue_load(j + 4, op);
+                } else if (op < kOps) {
+                    if (more) read_q(0, aa, ba, op - 2 * kLoads);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // Slices 0..3 in flight; wait for slice 0 (later slices may stay pending).
+    #pragma unroll
+    for (int t = 0; t < kStages; ++t)
+        if (t < T)
+            #pragma unroll
+            for (int i = 0; i < 2 * kLoads; ++i) issue_load(t, i);
+    if (T > 3) wait_vmcnt<6 * kLoads>();
+    else if (T > 2) wait_vmcnt<4 * kLoads>();
     else if (T > 1) wait_vmcnt<2 * kLoads>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    read(0, 0, 0);
-    for (int j = 0; j < T; ++j) {
-        lds_wait_all();                          // step (j, 0) fragments are in registers
-        read(1, j & (kStages - 1), 1);
-        mma(0);
-        if (j + 1 < T) {
-            // Slice j + 1 has landed when this thread's loads up to it are done
-            // (slice j + 2 may still be pending) and every wave has said so.
-            // Past the barrier every wave has also finished reading slice j - 1,
-            // whose stage slice j + 3 overwrites.
-            if (j + 2 < T) wait_vmcnt<2 * kLoads>();
+    {
+        const unsigned aa = frag_addr(0, 0, a_lane), ba = frag_addr(0, 0, b_lane);
+        #pragma unroll
+        for (int q = 0; q < kReads; ++q) read_q(0, aa, ba, q);
+    }
+    // Steady state: at the hand-off of slice j, slices j + 2 and j + 3 may
+    // still be in flight (2 x 2 kLoads loads of this thread).
+    int j = 0;
+    for (; j + 4 < T; ++j) slice(j, true, true, [] { wait_vmcnt<4 * kLoads>(); });
+    for (; j < T; ++j) {
+        const int after = T - 2 - j;          // slices issued after j + 1
+        slice(j, j + 1 < T, false, [&] {
+            if (after >= 2) wait_vmcnt<4 * kLoads>();
+            else if (after == 1) wait_vmcnt<2 * kLoads>();
             else wait_vmcnt<0>();
-            __builtin_amdgcn_s_barrier();
-            if (j + 3 < T) issue(j + 3);
-        }
-        lds_wait_all();                          // step (j, 1) fragments
-        if (j + 1 < T) read(0, (j + 1) & (kStages - 1), 0);
-        mma(1);
+        });
     }
 
     // Epilogue. acc[m][n][e] of lane l: hidden row 32 n + l % 32 of the wave's
