@@ -439,7 +439,8 @@ def run_lm_head(args, T, torch):
                    "hidden": x.d, "input_copies_rotated": len(copies)},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 1),
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": load_traffic("tree_lm_head_argmax_accept", args.workload),
                      "kernel": "tree_lm_head_argmax_accept",
                      "avg_us": round(t_call.mean() * 1e6, 2), "algorithmic_flop": flop,
                      "launches_per_call": 3},
