@@ -164,7 +164,8 @@ def test_lm_head_argument_checks(lib):
     assert lm(ws=NULL) == -1
     assert lm(d=0) == -2 and lm(d=48) == -2 and lm(d=16) == -2          # d: multiple of 32
     assert lm(V=0) == -2 and lm(N=257) == -2 and lm(B=65536) == -2
-    assert lm(B=65535, N=256, V=(1 << 31) - 1) == -2                    # grid above 2^31 - 1
+    assert lm(B=65535, N=256, V=(1 << 31) - 257) == -2                  # grid above 2^31 - 1
+    assert lm(B=1, N=1, V=(1 << 31) - 256) == -2                        # tile ids past 2^31 - 1
     assert lm(hidden=ctypes.c_void_p(0x10008)) == -3 and lm(w=ctypes.c_void_p(0x10008)) == -3
     assert lm(ws=ctypes.c_void_p(0x10004)) == -3
     need = lib.tv_lm_head_workspace_size(2, 64, 1000, 256)
