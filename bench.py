@@ -78,6 +78,28 @@ def compact_bytes(w, accept_len):
     return 2 * int(accept_len.sum()) * w.Hkv * w.D * 2 * 2    # K and V rows, read + write
 
 
+def warm_up(step, n_steps: int, min_seconds: float, torch):
+    """Run the W requested warm-up steps, then more until min_seconds have
+    passed (a short warm-up leaves the GPU below its sustained clocks); returns
+    the number of steps run. None of them is timed."""
+    t0 = time.perf_counter()
+    i = 0
+    while i < n_steps:
+        step(i)
+        i += 1
+    torch.cuda.synchronize()
+    while time.perf_counter() - t0 < min_seconds:
+        for _ in range(8):
+            step(i)
+            i += 1
+        torch.cuda.synchronize()
+    return i
+
+
+def pct(a, q):
+    return round(float(np.percentile(a, q)) * 1e6, 2)
+
+
 class TimingEvents:
     """HIP events used for timing only, created with hipEventDisableSystemFence:
     a default event makes a system-scope release (cache write-back) when it is
@@ -208,13 +230,24 @@ def write_traffic(workload: str, fetch_dir: str, write_dir: str, copy_fetch_dir:
                   f"{v['write_bytes'] / 1e6:8.2f} MB  ({v['dispatches']} dispatches)")
 
 
-def cpu_baseline(w, sample_b: int, min_seconds: float = 10.0):
-    """The fp64 CPU oracle on the first `sample_b` sequences of the same workload."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_step_rate(w, sl, min_seconds):
+    """Verified tree-tokens/s of the oracle's whole step on sequences `sl`,
+    repeated until about min_seconds of CPU work."""
     import oracle
-    sl = slice(0, sample_b)
     nn = None if w.num_nodes is None else w.num_nodes[sl]
     reps, t0 = 0, time.perf_counter()
-    while True:      # repeat the sample until about min_seconds of CPU work
+    while True:
         oracle.tree_attention(w.q[sl], w.k_tree[sl], w.v_tree[sl], w.k_cache, w.v_cache,
                               w.page_table[sl], w.kv_len[sl], w.parent[sl], num_nodes=nn)
         a = oracle.argmax(w.logits[sl])
@@ -226,10 +259,29 @@ def cpu_baseline(w, sample_b: int, min_seconds: float = 10.0):
         if dt >= min_seconds or reps >= 50:
             break
     tokens = int(real_nodes(w)[sl].sum())
-    return {"value": round(reps * tokens / dt, 2), "unit": "verified tree-tokens/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{sample_b} of {w.B} sequences of the same workload, {reps} passes "
-                      f"(fp64 C, OpenMP), {dt:.2f} s"}
+    return reps * tokens / dt, reps, dt
+
+
+def cpu_baseline(w, sample_b: int, min_seconds: float = 10.0, single_thread: bool = False):
+    """The fp64 CPU oracle on the first `sample_b` sequences of the same
+    workload, on every host thread; with `single_thread`, also on one."""
+    import oracle
+    sl = slice(0, sample_b)
+    threads = oracle.num_threads()
+    rate, reps, dt = _oracle_step_rate(w, sl, min_seconds)
+    out = {"value": round(rate, 2), "unit": "verified tree-tokens/s", "cores": threads,
+           "kind": "oracle", "cpu_model": cpu_model(),
+           "sample": f"{sample_b} of {w.B} sequences of the same workload, {reps} passes "
+                     f"(fp64 C, OpenMP, {threads} threads), {dt:.2f} s"}
+    if single_thread:
+        oracle.set_num_threads(1)
+        try:
+            rate1, reps1, dt1 = _oracle_step_rate(w, sl, min_seconds / 2)
+        finally:
+            oracle.set_num_threads(threads)
+        out["value_1_thread"] = round(rate1, 2)
+        out["sample_1_thread"] = f"the same sample on one thread, {reps1} passes, {dt1:.2f} s"
+    return out
 
 
 def tree_build_bytes(x, accept_len=None, r_min: int = 0) -> int:
@@ -286,16 +338,14 @@ def run_tree_build(args, T, torch):
                          num_nodes=o["nn"], workspace=ws)
         if ev: tev.record(ev[1], stream)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    warm_steps = warm_up(step, args.warmup, args.min_warmup_s, torch)
     ev_every = max(1, min(4, args.steps // 8))
     evs = [[tev.create() for _ in range(2)] if i % ev_every == 0 else None
            for i in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+        step(warm_steps + i, evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     sampled = [e for e in evs if e is not None]
@@ -322,7 +372,7 @@ def run_tree_build(args, T, torch):
             if dt >= 10.0 or reps >= 50:
                 break
         cpu = {"value": round(reps * nb / dt, 2), "unit": "draft trees/s", "cores": 1,
-               "kind": "oracle",
+               "kind": "oracle", "cpu_model": cpu_model(),
                "sample": f"{nb} of {x.B} sequences of the same workload, {reps} passes "
                          f"(numpy, one thread), {dt:.2f} s"}
     line = {
@@ -340,7 +390,8 @@ def run_tree_build(args, T, torch):
                      "traffic": load_traffic("tree_build", args.workload), "kernel": "tree_build",
                      "avg_us": round(t_call.mean() * 1e6, 2), "algorithmic_bytes": int(nbytes),
                      "launches_per_call": 2 * x.S + 2},
-        "call_us_p50": round(float(np.median(t_call)) * 1e6, 2),
+        "call_us_p10_p50_p90": [pct(t_call, 10), pct(t_call, 50), pct(t_call, 90)],
+        "warmup_steps_run": warm_steps,
         "timed_steps_with_events": len(sampled),
         "cpu_baseline": cpu,
         "source_digest": source_digest(),
@@ -379,16 +430,14 @@ def run_lm_head(args, T, torch):
                                      accept_idx=o["aidx"], bonus_token=o["bonus"], workspace=ws)
         if ev: tev.record(ev[1], stream)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    warm_steps = warm_up(step, args.warmup, args.min_warmup_s, torch)
     ev_every = max(1, min(4, args.steps // 8))
     evs = [[tev.create() for _ in range(2)] if i % ev_every == 0 else None
            for i in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+        step(warm_steps + i, evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     sampled = [e for e in evs if e is not None]
@@ -409,7 +458,7 @@ def run_lm_head(args, T, torch):
     for e in sampled:
         for q in e:
             tev.destroy(q)
-    alen = outs[(args.warmup + args.steps - 1) % len(copies)]["alen"].cpu().numpy()
+    alen = outs[(warm_steps + args.steps - 1) % len(copies)]["alen"].cpu().numpy()
     flop = 2.0 * R * x.V * x.d
     tflops = flop / t_call.mean() / 1e12
     cpu = None
@@ -425,7 +474,7 @@ def run_lm_head(args, T, torch):
                 break
         cpu = {"value": round(reps * nr / dt, 2), "unit": "verified tree-tokens/s",
                "cores": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)),
-               "kind": "oracle",
+               "kind": "oracle", "cpu_model": cpu_model(),
                "sample": f"LM-head argmax of the first {nr} of {R} node rows over the whole "
                          f"vocabulary, {reps} passes (numpy fp64 matmul), {dt:.2f} s"}
     line = {
@@ -444,7 +493,8 @@ def run_lm_head(args, T, torch):
                      "kernel": "tree_lm_head_argmax_accept",
                      "avg_us": round(t_call.mean() * 1e6, 2), "algorithmic_flop": flop,
                      "launches_per_call": 3},
-        "call_us_p50": round(float(np.median(t_call)) * 1e6, 2),
+        "call_us_p10_p50_p90": [pct(t_call, 10), pct(t_call, 50), pct(t_call, 90)],
+        "warmup_steps_run": warm_steps,
         "library_gemm_bf16_out_us": round(float(np.median(t_lib)) * 1e6, 2) if t_lib else None,
         "accept_len_hist": np.bincount(alen, minlength=1).tolist(),
         "timed_steps_with_events": len(sampled),
@@ -459,6 +509,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--min-warmup-s", type=float, default=1.5,
+                    help="keep warming up (untimed) until this many seconds have passed")
     ap.add_argument("--workload", default="llama8b_bs16")
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--cpu-sample", type=int, default=-1,
@@ -549,9 +601,7 @@ def main():
                               c["page_table"], c["kv_len"], o["aidx"], o["alen"])
         if ev: tev.record(ev[3], stream)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    warm_steps = warm_up(step, args.warmup, args.min_warmup_s, torch)
 
     # Even a fence-free event record costs the stream about a microsecond, so
     # the per-call durations are taken on every ev_every-th timed step only.
@@ -561,7 +611,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+        step(warm_steps + i, evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
@@ -576,30 +626,45 @@ def main():
     tokens = int(real_nodes(w).sum())
     value = tokens / (wall / args.steps)
 
-    alen = outs[0]["alen"].cpu().numpy()
+    alen = outs[(warm_steps + args.steps - 1) % len(copies)]["alen"].cpu().numpy()
     attn_bytes, attn_flop, acc_bytes = algorithmic(w)
     cmp_bytes = compact_bytes(w, alen)
     a_attn = attn_bytes / t_attn.mean() / 1e9
     a_acc = acc_bytes / t_acc.mean() / 1e9
 
-    def roof(kernel, bytes_, t, flop=None):
-        r = {"bound": "hbm", "achieved": round(bytes_ / t / 1e9, 1), "peak": HBM_PEAK_GBS,
-             "unit": "GB/s", "frac": round(bytes_ / t / 1e9 / HBM_PEAK_GBS, 4),
+    ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)     # FLOP per byte
+
+    def roof(kernel, bytes_, ts, flop=None):
+        """Roofline of one call from its per-call event times `ts`: HBM-bound
+        (GB/s against 8 TB/s) unless its algorithmic FLOP per byte is above the
+        ridge, then matrix-bound (TFLOP/s against the dense bf16 peak)."""
+        t = ts.mean()
+        gbs = bytes_ / t / 1e9
+        r = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+             "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
              "traffic": load_traffic(kernel, args.workload),
-             "kernel": kernel, "avg_us": round(t * 1e6, 2), "algorithmic_bytes": int(bytes_)}
+             "kernel": kernel, "avg_us": round(t * 1e6, 2), "p10_us": pct(ts, 10),
+             "p50_us": pct(ts, 50), "p90_us": pct(ts, 90), "algorithmic_bytes": int(bytes_)}
         if flop is not None:
-            r["tflops"] = round(flop / t / 1e12, 1)
-            r["mfma_frac"] = round(flop / t / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+            tf = flop / t / 1e12
+            r["tflops"] = round(tf, 1)
+            r["mfma_frac"] = round(tf / MFMA_BF16_PEAK_TFLOPS, 4)
+            r["hbm_gbs"] = round(gbs, 1)
+            r["hbm_frac"] = round(gbs / HBM_PEAK_GBS, 4)
+            r["algorithmic_flop"] = int(flop)
+            if flop / bytes_ > ridge:
+                r.update(bound="mfma", achieved=round(tf, 1), peak=MFMA_BF16_PEAK_TFLOPS,
+                         unit="TFLOP/s", frac=round(tf / MFMA_BF16_PEAK_TFLOPS, 4))
         return r
 
-    r_attn = roof("tree_verify_attention", attn_bytes, t_attn.mean(), attn_flop)
-    r_acc = roof("tree_argmax_accept", acc_bytes, t_acc.mean())
+    r_attn = roof("tree_verify_attention", attn_bytes, t_attn, attn_flop)
+    r_acc = roof("tree_argmax_accept", acc_bytes, t_acc)
     dominant = r_acc if t_acc.mean() >= t_attn.mean() else r_attn
 
     cpu = None
     if args.cpu_sample != 0:
         nb = w.B if args.cpu_sample < 0 else min(args.cpu_sample, w.B)
-        cpu = cpu_baseline(w, nb)
+        cpu = cpu_baseline(w, nb, single_thread=args.workload in ("tiny", "llama8b_bs1"))
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "verified tree-tokens/s",
@@ -617,9 +682,14 @@ def main():
         "step_breakdown_us": {"attention": round(t_attn.mean() * 1e6, 2),
                               "argmax_accept": round(t_acc.mean() * 1e6, 2),
                               "compact": round(t_cmp.mean() * 1e6, 2),
-                              "attention_p50": round(float(np.median(t_attn)) * 1e6, 2),
-                              "argmax_accept_p50": round(float(np.median(t_acc)) * 1e6, 2),
+                              "attention_p10_p50_p90": [pct(t_attn, 10), pct(t_attn, 50),
+                                                        pct(t_attn, 90)],
+                              "argmax_accept_p10_p50_p90": [pct(t_acc, 10), pct(t_acc, 50),
+                                                            pct(t_acc, 90)],
+                              "compact_p10_p50_p90": [pct(t_cmp, 10), pct(t_cmp, 50),
+                                                      pct(t_cmp, 90)],
                               "timed_steps_with_events": len(sampled)},
+        "warmup_steps_run": warm_steps,
         "kernel_tokens_per_s": round(tokens / (t_attn.mean() + t_acc.mean() + t_cmp.mean()), 1),
         "accept_len_hist": np.bincount(alen).tolist(),
         "compact_bytes": cmp_bytes,

@@ -56,6 +56,8 @@ def _load():
         lib.oracle_kv_compact.restype = i
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = i
+        lib.oracle_set_num_threads.argtypes = [i]
+        lib.oracle_set_num_threads.restype = None
         _lib = lib
     return _lib
 
@@ -87,6 +89,11 @@ def num_threads() -> int:
     return int(_load().oracle_num_threads())
 
 
+def set_num_threads(n: int) -> None:
+    """Threads of the OpenMP loops from now on (results do not depend on it)."""
+    _load().oracle_set_num_threads(int(n))
+
+
 def tree_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent,
                    scale: float = 0.0, num_nodes=None):
     """Tree-masked attention (§2.1 tree-shaped verification mask; §8 SpecInfer
@@ -114,6 +121,8 @@ def tree_attention(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, pare
         _ptr(q), _ptr(k_tree), _ptr(v_tree), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
         _ptr(kv_len), _ptr(parent), _optr(nn), B, N, Hq, Hkv, D, P, max_pages, num_pages,
         float(scale), _ptr(out), _ptr(lse))
+    if rc == -2:
+        raise MemoryError("oracle_tree_attention: scratch allocation failed")
     if rc != 0:
         raise ValueError("oracle_tree_attention rejected its arguments")
     return out, lse
@@ -142,6 +151,8 @@ def tree_attention_rows(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len,
         _ptr(q), _ptr(k_tree), _ptr(v_tree), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
         _ptr(kv_len), _ptr(parent), _optr(nn), B, N, Hq, Hkv, D, P, page_table.shape[1], num_pages,
         float(scale), _ptr(items), len(items), _ptr(out), _ptr(lse))
+    if rc == -2:
+        raise MemoryError("oracle_tree_attention_rows: scratch allocation failed")
     if rc != 0:
         raise ValueError("oracle_tree_attention_rows rejected its arguments")
     return out, lse
@@ -173,6 +184,8 @@ def accept(draft, parent, amax, num_nodes=None):
     bonus = np.zeros(B, dtype=np.int32)
     rc = _load().oracle_accept(_ptr(draft), _ptr(parent), _ptr(amax), _optr(nn), B, N,
                                _ptr(alen), _ptr(aidx), _ptr(bonus))
+    if rc == -2:
+        raise MemoryError("oracle_accept: scratch allocation failed")
     if rc != 0:
         raise ValueError("oracle_accept: parent[i] must lie in [-1, i-1]")
     return alen, aidx, bonus

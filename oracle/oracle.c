@@ -66,6 +66,17 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Threads the OpenMP loops below use from now on (results do not depend on it). */
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Node count of sequence b: num_nodes[b] when given, else N. */
 static int nodes_of(const int32_t *num_nodes, int N, int b)
 {
@@ -112,8 +123,9 @@ static void padding_row(int D, double *o, double *lse_out)
 }
 
 /* One output row: node i of sequence b, query head h. Writes D values to o
- * and the log-sum-exp to *lse_out (if not NULL). */
-static void attend_one(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
+ * and the log-sum-exp to *lse_out (if not NULL). Returns 0, or -1 when its
+ * scratch memory cannot be allocated (nothing written). */
+static int attend_one(const uint16_t *q, const uint16_t *k_tree, const uint16_t *v_tree,
                        const uint16_t *k_cache, const uint16_t *v_cache,
                        const int32_t *page_table, const int32_t *kv_len, const int32_t *parent,
                        int N, int Hq, int Hkv, int D, int P, int max_pages, double scale, int b,
@@ -131,6 +143,12 @@ static void attend_one(const uint16_t *q, const uint16_t *k_tree, const uint16_t
     const uint16_t **krow = malloc(sizeof(*krow) * (size_t)nvis);
     const uint16_t **vrow = malloc(sizeof(*vrow) * (size_t)nvis);
     double *s = malloc(sizeof(double) * (size_t)nvis);
+    if (!krow || !vrow || !s) {
+        free(krow);
+        free(vrow);
+        free(s);
+        return -1;
+    }
 
     int n = 0;
     for (int t = 0; t < L; ++t) {
@@ -163,17 +181,21 @@ static void attend_one(const uint16_t *q, const uint16_t *k_tree, const uint16_t
         s[j] = exp(s[j] - m);
         denom += s[j];
     }
-    for (int d = 0; d < D; ++d) {
-        double acc = 0.0;
-        for (int j = 0; j < n; ++j)
-            acc += s[j] * widen_bf16(vrow[j][d]);
-        o[d] = acc / denom;
-    }
+    /* o[d] = sum_j s_j v_j[d] / denom; each o[d] sums its terms in key order
+     * j = 0, 1, ..., walking the value rows one after the other */
+    for (int d = 0; d < D; ++d)
+        o[d] = 0.0;
+    for (int j = 0; j < n; ++j)
+        for (int d = 0; d < D; ++d)
+            o[d] += s[j] * widen_bf16(vrow[j][d]);
+    for (int d = 0; d < D; ++d)
+        o[d] /= denom;
     if (lse_out)
         *lse_out = m + log(denom);
     free(krow);
     free(vrow);
     free(s);
+    return 0;
 }
 
 /* Tree-masked attention of every node's query heads over the paged prefix
@@ -196,6 +218,7 @@ int oracle_tree_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
     if (!(scale > 0.0))
         scale = 1.0 / sqrt((double)D);
 
+    int failed = 0;
 #pragma omp parallel for collapse(3) schedule(dynamic, 4)
     for (int b = 0; b < B; ++b)
         for (int i = 0; i < N; ++i)
@@ -203,12 +226,14 @@ int oracle_tree_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
                 long row = ((long)b * N + i) * Hq + h;
                 if (i >= nodes_of(num_nodes, N, b))
                     padding_row(D, out + row * D, lse ? lse + row : NULL);
-                else
-                    attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent,
-                               N, Hq, Hkv, D, P, max_pages, scale, b, i, h, out + row * D,
-                               lse ? lse + row : NULL);
+                else if (attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len,
+                                    parent, N, Hq, Hkv, D, P, max_pages, scale, b, i, h,
+                                    out + row * D, lse ? lse + row : NULL) != 0) {
+#pragma omp atomic write
+                    failed = 1;
+                }
             }
-    return 0;
+    return failed ? -2 : 0;
 }
 
 /* The same attention for a list of n_items (b, i, h) triples only (items is
@@ -233,17 +258,20 @@ int oracle_tree_attention_rows(const uint16_t *q, const uint16_t *k_tree, const 
     if (!(scale > 0.0))
         scale = 1.0 / sqrt((double)D);
 
+    int failed = 0;
 #pragma omp parallel for schedule(dynamic, 1)
     for (int k = 0; k < n_items; ++k) {
         const int32_t *it = items + 3L * k;
         if (it[1] >= nodes_of(num_nodes, N, it[0]))
             padding_row(D, out_rows + (long)k * D, lse_rows ? lse_rows + k : NULL);
-        else
-            attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, N, Hq,
-                       Hkv, D, P, max_pages, scale, it[0], it[1], it[2], out_rows + (long)k * D,
-                       lse_rows ? lse_rows + k : NULL);
+        else if (attend_one(q, k_tree, v_tree, k_cache, v_cache, page_table, kv_len, parent, N,
+                            Hq, Hkv, D, P, max_pages, scale, it[0], it[1], it[2],
+                            out_rows + (long)k * D, lse_rows ? lse_rows + k : NULL) != 0) {
+#pragma omp atomic write
+            failed = 1;
+        }
     }
-    return 0;
+    return failed ? -2 : 0;
 }
 
 /* argmax over each of `rows` rows of V fp32 logits: the lowest index holding
@@ -292,6 +320,11 @@ int oracle_accept(const int32_t *draft, const int32_t *parent, const int32_t *am
         }
         int *acc = malloc(sizeof(int) * (size_t)N);
         int *depth = malloc(sizeof(int) * (size_t)N);
+        if (!acc || !depth) {
+            free(acc);
+            free(depth);
+            return -2;
+        }
         int sel = -1;
         for (int i = 0; i < nb; ++i) {
             int p = par[i];

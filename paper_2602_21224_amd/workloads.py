@@ -146,6 +146,39 @@ def tree_topk_expansion(rng: np.random.Generator, branching, keep: int):
     return parent
 
 
+def tree_frontier_expansion(rng: np.random.Generator, k: int, steps: int, keep: int):
+    """A draft tree the way the paper's evaluation verifies them (§7.1: trees
+    of depth 3 at most 4 wide): from the root, each of `steps` levels offers k
+    children to every frontier node (probabilities: the top-k entries of a
+    sorted Dirichlet(1 x 8) draw), and the k children of largest joint
+    probability form the next frontier. The root and the frontier nodes of
+    every level make an ancestor-closed tree at most k wide; the `keep` of
+    largest joint probability (ties to the node created first) are kept, in
+    creation order. Only shapes the synthetic input; returns the parent array."""
+    par = [-1]
+    joint = [1.0]
+    frontier = [0]
+    members = [0]
+    for _ in range(steps):
+        cand = []
+        for node in frontier:
+            for pr in np.sort(rng.dirichlet(np.ones(8)))[::-1][:k]:
+                par.append(node)
+                joint.append(joint[node] * float(pr))
+                cand.append(len(par) - 1)
+        frontier = sorted(cand, key=lambda i: (-joint[i], i))[:k]
+        members += sorted(frontier)
+    kept = sorted(sorted(members, key=lambda i: (-joint[i], i))[:keep])
+    relabel = {old: new for new, old in enumerate(kept)}
+    parent = np.empty(len(kept), dtype=np.int32)
+    for new, old in enumerate(kept):
+        p = par[old]
+        if p >= 0 and p not in relabel:
+            raise AssertionError("pruned tree is not ancestor-closed")
+        parent[new] = -1 if p < 0 else relabel[p]
+    return parent
+
+
 def fusion_forest(rng: np.random.Generator, primary, resampled, depth_lt: int) -> np.ndarray:
     """Input of a fused verification (§6.2: the previous round's re-sampled
     trees are verified together with the next batch): this round's draft tree
@@ -338,12 +371,20 @@ PRESETS = ("tiny", "llama8b_bs1", "llama8b_bs16", "llama70b_bs8", "long_wide_bs4
 # Ragged forests of a fused verification (this round's tree plus the previous
 # round's re-sampled tree per sequence, padded to N).
 RAGGED_PRESETS = ("llama8b_bs16_fused",)
+# The paper's own verification shape (§7.1: LLaMA-2-7B, multi-head attention,
+# depth-3 trees at most 4 wide, 12 tokens verified per request, batches 2-16).
+PAPER_PRESETS = ("llama2_7b_bs2", "llama2_7b_bs16")
 
 
 def preset(name: str, *, poison: bool = False, with_logits: bool = True,
-           B: int | None = None, boost_amount: float = 3.0) -> Workload:
+           B: int | None = None, boost_amount: float = 3.0,
+           boost_prob: float | None = None) -> Workload:
     """The five Llama-shaped verification workloads. Preset k (1-based) uses
-    seed k-1. `B` overrides the batch (a bounded sample of the same recipe)."""
+    seed k-1. `B` overrides the batch (a bounded sample of the same recipe);
+    `boost_amount` and `boost_prob` override the draft-token boost (tests use
+    +20 with probability 1 to force deep accepted paths)."""
+    def bp(default):
+        return default if boost_prob is None else boost_prob
     if name == "tiny":
         return make_workload(name, 0, B=B or 1, N=16, Hq=8, Hkv=8, D=64, kv_len=128,
                              parent_fn=lambda r: tree_uniform_forest(r, 16), V=1000,
@@ -352,30 +393,37 @@ def preset(name: str, *, poison: bool = False, with_logits: bool = True,
     if name == "llama8b_bs1":
         return make_workload(name, 1, B=B or 1, N=64, Hq=32, Hkv=8, D=128, kv_len=2048,
                              parent_fn=lambda r: tree_topk_expansion(r, (4, 4, 2, 2, 1, 1), 64),
-                             V=128256, boost_prob=0.6, boost_amount=boost_amount,
+                             V=128256, boost_prob=bp(0.6), boost_amount=boost_amount,
                              poison=poison, with_logits=with_logits)
     if name == "llama8b_bs16":
         return make_workload(name, 2, B=B or 16, N=64, Hq=32, Hkv=8, D=128,
                              kv_len=(1024, 4096),
                              parent_fn=lambda r: tree_random_depth_capped(r, 64, 8),
-                             V=128256, boost_prob=0.6, boost_amount=boost_amount,
+                             V=128256, boost_prob=bp(0.6), boost_amount=boost_amount,
                              poison=poison, with_logits=with_logits)
     if name == "llama70b_bs8":
         return make_workload(name, 3, B=B or 8, N=128, Hq=64, Hkv=8, D=128, kv_len=8192,
                              parent_fn=lambda r: tree_random_depth_capped(r, 128, 10),
-                             V=128256, boost_prob=0.5, boost_amount=boost_amount,
+                             V=128256, boost_prob=bp(0.5), boost_amount=boost_amount,
                              poison=poison, with_logits=with_logits)
     if name == "llama8b_bs16_fused":
         return make_workload(name, 5, B=B or 16, N=64, Hq=32, Hkv=8, D=128,
                              kv_len=(1024, 4096),
                              parent_fn=lambda r: fusion_forest(r, (24, 48), (0, 16), 8),
-                             V=128256, boost_prob=0.6, boost_amount=boost_amount,
+                             V=128256, boost_prob=bp(0.6), boost_amount=boost_amount,
+                             poison=poison, with_logits=with_logits)
+    if name in ("llama2_7b_bs2", "llama2_7b_bs16"):
+        return make_workload(name, 6 if name.endswith("bs2") else 7,
+                             B=B or (2 if name.endswith("bs2") else 16), N=12, Hq=32, Hkv=32,
+                             D=128, kv_len=(256, 2048),
+                             parent_fn=lambda r: tree_frontier_expansion(r, 4, 3, 12),
+                             V=32000, boost_prob=bp(0.6), boost_amount=boost_amount,
                              poison=poison, with_logits=with_logits)
     if name == "long_wide_bs4":
         return make_workload(name, 4, B=B or 4, N=256, Hq=32, Hkv=8, D=128, kv_len=32768,
                              parent_fn=lambda r: tree_random_depth_capped(r, 256, 12,
                                                                           root_children=8),
-                             V=128256, boost_prob=0.4, boost_amount=boost_amount,
+                             V=128256, boost_prob=bp(0.4), boost_amount=boost_amount,
                              poison=poison, with_logits=with_logits)
     raise KeyError(name)
 
@@ -391,6 +439,10 @@ PRESET_DOC = {
                     "(depth <= 10), vocab 128256, +3 boost w.p. 0.5",
     "long_wide_bs4": "batch 4, 32/8 heads, head_dim 128, prefix 32768, 256-node trees "
                      "(8 root children, depth <= 12), vocab 128256, +3 boost w.p. 0.4",
+    "llama2_7b_bs2": "batch 2, 32/32 heads (MHA), head_dim 128, prefix U[256,2048], 12-node "
+                     "trees of depth 3 at most 4 wide, vocab 32000, +3 boost w.p. 0.6, seed 6",
+    "llama2_7b_bs16": "batch 16, 32/32 heads (MHA), head_dim 128, prefix U[256,2048], 12-node "
+                      "trees of depth 3 at most 4 wide, vocab 32000, +3 boost w.p. 0.6, seed 7",
     "llama8b_bs16_fused": "batch 16, 32/8 heads, head_dim 128, prefix U[1024,4096], per "
                           "sequence a 24-48-node tree plus a 0-16-node re-sampled tree "
                           "(second root), padded to 64, vocab 128256, seed 5",

@@ -28,10 +28,10 @@ def check_accept(oracle_mod, T, logits, draft, parent, label):
     np.testing.assert_array_equal(bonus, rb)
     hist = np.bincount(alen)
     print(f"[{label}] accept_len histogram {hist.tolist()}", flush=True)
-    return alen, aidx
+    return a, alen, aidx
 
 
-@pytest.mark.parametrize("name", W.PRESETS)
+@pytest.mark.parametrize("name", W.PRESETS + W.PAPER_PRESETS)
 def test_presets(oracle_mod, name):
     T = U.require_gpu()
     w = W.preset(name)
@@ -46,8 +46,8 @@ def test_forced_deep_paths(oracle_mod):
     w2 = W.make_workload("forced", 9, B=8, N=64, Hq=1, Hkv=1, D=64, kv_len=10,
                          parent_fn=lambda r: W.tree_random_depth_capped(r, 64, 8), V=5000,
                          boost_prob=1.0, boost_amount=20.0)
-    alen, _ = check_accept(oracle_mod, T, w.logits, w.draft, w.parent, "boost20")
-    alen2, _ = check_accept(oracle_mod, T, w2.logits, w2.draft, w2.parent, "boost20-small")
+    check_accept(oracle_mod, T, w.logits, w.draft, w.parent, "boost20")
+    _, alen2, _ = check_accept(oracle_mod, T, w2.logits, w2.draft, w2.parent, "boost20-small")
     assert alen2.max() >= 4
 
 
@@ -108,13 +108,19 @@ def _compact_case(oracle_mod, T, w, alen, aidx, label):
     assert np.array_equal(got_k, rk) and np.array_equal(got_v, rv)
 
 
-def test_compaction_after_accept(oracle_mod):
+@pytest.mark.parametrize("name", W.PRESETS + W.PAPER_PRESETS)
+def test_accept_then_compaction_forced_paths(oracle_mod, name):
+    """Every preset with a +20 boost on one child of every internal node, so
+    accepted paths run down to the trees' depth caps: the GPU's argmax/accept
+    must equal the oracle's, and the GPU's compaction of the GPU's accepted
+    paths must equal the oracle's compaction byte for byte."""
     T = U.require_gpu()
-    for name in ("tiny", "llama8b_bs16"):
-        w = W.preset(name, poison=True, boost_amount=20.0)
-        a = oracle_mod.argmax(w.logits)
-        alen, aidx, _ = oracle_mod.accept(w.draft, w.parent, a)
-        _compact_case(oracle_mod, T, w, alen, aidx, name)
+    w = W.preset(name, poison=True, boost_amount=20.0, boost_prob=1.0)
+    _, alen, aidx = check_accept(oracle_mod, T, w.logits, w.draft, w.parent, f"{name}+20")
+    if name != "tiny":
+        deep = min(5, max(w.meta["max_depth"]) + 1)
+        assert alen.max() >= deep, f"{name}: the forced boosts should give deep paths"
+    _compact_case(oracle_mod, T, w, alen, aidx, name)
 
 
 def test_compaction_crosses_pages_and_len_one(oracle_mod):

@@ -1,9 +1,10 @@
 """GPU parity of tree_verify_attention against the CPU oracle (through the C ABI).
 
-Small shapes are compared element by element on every output; the full-size
-Llama-shaped workloads run in the same launch configuration the benchmark
-times and are compared on sampled (sequence, node, head) rows the oracle
-computes one by one, plus properties that hold at any size.
+Every output (out and lse) is compared element by element with the oracle,
+on small shapes and on the five Llama-shaped workloads at full size, in the
+launch configuration the benchmark times; properties that hold at any size
+(determinism, page-permutation invariance, no leakage from invisible tree
+rows) are checked on top.
 """
 import numpy as np
 import pytest
@@ -85,31 +86,35 @@ def test_llama8b_bs1_preset_all_outputs(oracle_mod):
                  "llama8b_bs1")
 
 
-def _sampled(oracle_mod, T, w, n_rows, seed, label):
-    print(f"case {label}: sampled {n_rows} rows", flush=True)
-    got, glse = U.gpu_attention(T, w)
-    rng = np.random.default_rng(seed)
-    items = np.stack([rng.integers(0, w.B, n_rows), rng.integers(0, w.N, n_rows),
-                      rng.integers(0, w.Hq, n_rows)], 1).astype(np.int32)
-    # always include the last node and the root of the longest sequence, every head of one node
-    b_long = int(np.argmax(w.kv_len))
-    extra = [(b_long, w.N - 1, h) for h in range(w.Hq)] + [(b_long, 0, 0), (0, 0, w.Hq - 1)]
-    items = np.concatenate([items, np.array(extra, np.int32)])
-    want, wlse = oracle_mod.tree_attention_rows(w.q, w.k_tree, w.v_tree, w.k_cache, w.v_cache,
-                                                w.page_table, w.kv_len, w.parent, items)
-    g = got[items[:, 0], items[:, 1], items[:, 2]]
-    gl = glse[items[:, 0], items[:, 1], items[:, 2]]
-    U.assert_attention_close(g, want, gl, wlse, label)
-    assert np.isfinite(got).all() and np.isfinite(glse).all()
-    return got
-
-
-@pytest.mark.parametrize("name,rows", [("llama8b_bs16", 384), ("llama70b_bs8", 160),
-                                       ("long_wide_bs4", 48)])
-def test_full_size_presets_sampled(oracle_mod, name, rows):
+@pytest.mark.parametrize("name", ["llama8b_bs16", "llama70b_bs8", "long_wide_bs4"])
+def test_full_size_presets_all_outputs(oracle_mod, name):
+    """Configs 3-5 at full size: every out and lse element against the oracle."""
     T = U.require_gpu()
     w = W.preset(name, poison=True, with_logits=False)
-    _sampled(oracle_mod, T, w, rows, 11, name)
+    full_compare(oracle_mod, T, w, name)
+
+
+@pytest.mark.parametrize("name", W.PAPER_PRESETS)
+def test_paper_shape_presets_all_outputs(oracle_mod, name):
+    """The paper's own verification shape (multi-head attention, 12-node trees of
+    depth 3 at most 4 wide): 12 query rows per KV head."""
+    T = U.require_gpu()
+    w = W.preset(name, poison=True, with_logits=False)
+    full_compare(oracle_mod, T, w, name)
+
+
+@pytest.mark.parametrize("B,N,Hq,Hkv,L,P", [
+    (2, 12, 8, 2, (1500, 3000), 1),    # pages of one key: a 512-key page-id window
+    (2, 9, 8, 2, (1600, 2900), 2),     # pages of two keys: 1024-key windows
+    (1, 16, 16, 4, 9000, 16),          # 16-key pages: crosses the 8192-key window once
+])
+def test_page_id_windows(oracle_mod, B, N, Hq, Hkv, L, P):
+    """Pieces whose prefix spans more page ids than the kernel caches at once run in
+    several windows that carry the softmax state across; every output crosses at
+    least one window boundary."""
+    T = U.require_gpu()
+    w = wl(71 + P, B=B, N=N, Hq=Hq, Hkv=Hkv, D=128, L=L, P=P, tree="capped")
+    full_compare(oracle_mod, T, w, f"window_P{P}")
 
 
 def test_page_permutation_and_determinism():

@@ -81,11 +81,22 @@ def test_tree_build_narrative(oracle_mod):
 
 
 def test_tree_build_full_vocabulary(oracle_mod):
-    """The 8B-shaped vocabulary (128256) at the bench's tree parameters, with
-    a quarter of the hot table (8192 hot tokens) to keep the CPU side short."""
+    """The 8B-shaped vocabulary (128256) with a quarter of the hot table (8192
+    hot tokens)."""
     T = U.require_gpu()
     x = W.make_tree_build_inputs("full", 7, B=4, S=7, V=128256, H=8192, k=8, budget=64)
     compare(oracle_mod, T, x, "full-vocab")
+
+
+def test_tree_build_and_resample_bench_presets(oracle_mod):
+    """The benchmarked workloads themselves, whole: 16 sequences, 7 steps,
+    vocabulary 128256 with 32768 hot tokens, k 8, budget 64; then re-sampling
+    on the same inputs with the benchmark's accept lengths and bonus tokens."""
+    T = U.require_gpu()
+    x = W.tree_build_preset("tb_llama8b_bs16")
+    compare(oracle_mod, T, x, "tb_llama8b_bs16")
+    bonus, alen = W.resample_inputs(x, 7)
+    compare_resample(oracle_mod, T, x, bonus, alen, 1, "rs_llama8b_bs16-shapes")
 
 
 def test_tree_build_feeds_verification(oracle_mod):
