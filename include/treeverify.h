@@ -73,7 +73,10 @@ extern "C" {
 #define TV_API
 #endif
 
-#define TV_ABI_VERSION 4
+#define TV_ABI_VERSION 5
+
+/* Size of the static device scratch of tree_argmax_accept_noalloc (per GPU). */
+#define TV_NOALLOC_SCRATCH_BYTES (4u << 20)
 
 enum tv_status {
     TV_OK = 0,
@@ -82,7 +85,8 @@ enum tv_status {
     TV_ERR_ALIGN = -3,       /* a tensor pointer is not 16-byte aligned         */
     TV_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required      */
     TV_ERR_HIP = -5,         /* a HIP runtime call or kernel launch failed      */
-    TV_ERR_DEVICE = -6       /* the current device is not gfx950                */
+    TV_ERR_DEVICE = -6,      /* the current device is not gfx950                */
+    TV_ERR_SCRATCH = -7      /* more scratch needed than the static buffer holds */
 };
 
 /* TV_ABI_VERSION of the built library. */
@@ -181,6 +185,31 @@ TV_API int tree_argmax_accept(const float *logits, const int32_t *draft_tokens,
                               int V, int32_t *argmax_out,
                               int32_t *accept_len, int32_t *accept_idx, int32_t *bonus_token,
                               void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * tree_argmax_accept_noalloc
+ *
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): exactly
+ * tree_argmax_accept (same arguments apart from the workspace, same kernels,
+ * same results), with its per-(node, vocabulary segment) keys kept in a static
+ * device buffer of TV_NOALLOC_SCRATCH_BYTES (4 MiB) that the library holds on
+ * every GPU it runs on until the process ends. The call allocates nothing:
+ * the buffer's device address is looked up once per device on the first call
+ * (hipGetSymbolAddress, no allocation). Every key the call reads is written
+ * earlier in the same call, so nothing needs clearing between calls.
+ *
+ * Limit: tv_argmax_workspace_size(B, N, V) <= TV_NOALLOC_SCRATCH_BYTES
+ * (B * N <= 524256 node rows, whatever V); larger batches return
+ * TV_ERR_SCRATCH and launch nothing. All calls on one GPU share its buffer:
+ * calls that can overlap in time on one GPU (several streams, several host
+ * threads) race on it and must be serialised by the caller.
+ * ------------------------------------------------------------------------ */
+TV_API int tree_argmax_accept_noalloc(const float *logits, const int32_t *draft_tokens,
+                                      const int32_t *parent, const int32_t *num_nodes, int B,
+                                      int N, int V, int32_t *argmax_out, int32_t *accept_len,
+                                      int32_t *accept_idx, int32_t *bonus_token,
+                                      hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * kv_compact_accepted

@@ -46,6 +46,8 @@ def load():
     lib.tv_argmax_workspace_size.restype = sz
     lib.tree_argmax_accept.argtypes = [p] * 4 + [i] * 3 + [p] * 5 + [sz, p]
     lib.tree_argmax_accept.restype = i
+    lib.tree_argmax_accept_noalloc.argtypes = [p] * 4 + [i] * 3 + [p] * 5
+    lib.tree_argmax_accept_noalloc.restype = i
     lib.kv_compact_accepted.argtypes = [p] * 8 + [i] * 7 + [p]
     lib.kv_compact_accepted.restype = i
     lib.tv_validate_inputs.argtypes = [p] * 4 + [i] * 5 + [p, p]
@@ -177,6 +179,27 @@ def tree_argmax_accept(logits, draft_tokens, parent, *, num_nodes=None, argmax_o
         _ptr(accept_len), _ptr(accept_idx), _ptr(bonus_token), _ptr(workspace),
         workspace.numel(), _stream(stream))
     _check(st, "tree_argmax_accept")
+    return argmax_out, accept_len, accept_idx, bonus_token
+
+
+def tree_argmax_accept_noalloc(logits, draft_tokens, parent, *, argmax_out, accept_len,
+                               accept_idx, bonus_token, num_nodes=None, stream=None):
+    """tree_argmax_accept with the library's static per-GPU scratch instead of a
+    workspace: nothing is allocated, so every output tensor must be given.
+    Calls that can overlap on one GPU race on that scratch."""
+    B, N, V = logits.shape
+    _want(logits, "logits", (torch.float32,))
+    _want(draft_tokens, "draft_tokens", (torch.int32,), (B, N))
+    _want(parent, "parent", (torch.int32,), (B, N))
+    if num_nodes is not None:
+        _want(num_nodes, "num_nodes", (torch.int32,), (B,))
+    for t, n, s in ((argmax_out, "argmax_out", (B, N)), (accept_len, "accept_len", (B,)),
+                    (accept_idx, "accept_idx", (B, N)), (bonus_token, "bonus_token", (B,))):
+        _want(t, n, (torch.int32,), s)
+    st = load().tree_argmax_accept_noalloc(
+        _ptr(logits), _ptr(draft_tokens), _ptr(parent), _ptr(num_nodes), B, N, V,
+        _ptr(argmax_out), _ptr(accept_len), _ptr(accept_idx), _ptr(bonus_token), _stream(stream))
+    _check(st, "tree_argmax_accept_noalloc")
     return argmax_out, accept_len, accept_idx, bonus_token
 
 

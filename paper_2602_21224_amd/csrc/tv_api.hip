@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
+
 #define TREEVERIFY_BUILD 1
 #include "treeverify.h"
 #include "tv_internal.h"
@@ -20,6 +22,27 @@ constexpr int kArgmaxMinSegment = 4096;
 
 int g_cu_count[kMaxDevices];         // 0 = not yet queried
 int g_is_gfx950[kMaxDevices];        // 0 = not yet queried, 1 = yes, -1 = no
+
+// Scratch of tree_argmax_accept_noalloc: one copy per GPU, held until the
+// process ends. Host code never names it directly (its host-side name is a
+// stand-in, not a device address); it uses the per-device address that
+// hipGetSymbolAddress returns, looked up once per device on the first call.
+static __device__ __align__(256) unsigned char scratch[TV_NOALLOC_SCRATCH_BYTES];
+std::atomic<void *> g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch, or nullptr if the lookup fails.
+void *scratch_ptr() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    void *ptr = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (ptr == nullptr) {
+        // Two threads may race here; both store the same address.
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr)
+            return nullptr;
+        g_scratch_ptr[dev].store(ptr, std::memory_order_release);
+    }
+    return ptr;
+}
 
 bool device_ok() {
     int dev = 0;
@@ -126,6 +149,9 @@ const char *tv_status_string(int status) {
         case TV_ERR_WORKSPACE: return "workspace missing or smaller than required";
         case TV_ERR_HIP: return "a HIP runtime call or kernel launch failed";
         case TV_ERR_DEVICE: return "the current device is not gfx950";
+        case TV_ERR_SCRATCH:
+            return "the call needs more scratch than the library's static buffer holds "
+                   "(TV_NOALLOC_SCRATCH_BYTES)";
         default: return "unknown status";
     }
 }
@@ -204,27 +230,75 @@ size_t tv_argmax_workspace_size(int B, int N, int V) {
     return round_up((size_t)B * N * segs * sizeof(unsigned long long), 256) + 256;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Argument checks and launches shared by tree_argmax_accept and its no-alloc
+// variant; `ws` is the per-(row, segment) key buffer (every slot the accept
+// kernel reads is written earlier in the same call).
+int argmax_accept_checked(const float *logits, const int32_t *draft_tokens, const int32_t *parent,
+                          const int32_t *num_nodes, int B, int N, int V, int32_t *argmax_out,
+                          int32_t *accept_len, int32_t *accept_idx, int32_t *bonus_token,
+                          void *ws, hipStream_t stream) {
+    int segs = 1, seg_len = 4;
+    argmax_plan(B, N, V, &segs, &seg_len);
+    const hipError_t e = tv::launch_argmax_accept(
+        logits, draft_tokens, parent, num_nodes, B, N, V, segs, seg_len, argmax_out, accept_len,
+        accept_idx, bonus_token, static_cast<unsigned long long *>(ws), stream);
+    return e == hipSuccess ? TV_OK : TV_ERR_HIP;
+}
+
+bool argmax_args_ok(int B, int N, int V) {
+    return B >= 0 && B <= 65535 && N >= 1 && N <= tv::kMaxNodes && V >= 1;
+}
+
+bool argmax_ptrs_ok(const float *logits, const int32_t *draft_tokens, const int32_t *parent,
+                    int32_t *argmax_out, int32_t *accept_len, int32_t *accept_idx,
+                    int32_t *bonus_token) {
+    return logits && draft_tokens && parent && argmax_out && accept_len && accept_idx &&
+           bonus_token;
+}
+
+}  // namespace
+
+extern "C" {
+
 int tree_argmax_accept(const float *logits, const int32_t *draft_tokens, const int32_t *parent,
                        const int32_t *num_nodes, int B, int N, int V, int32_t *argmax_out,
                        int32_t *accept_len,
                        int32_t *accept_idx, int32_t *bonus_token, void *workspace,
                        size_t workspace_bytes, hipStream_t stream) {
-    if (B < 0 || B > 65535 || N < 1 || N > tv::kMaxNodes || V < 1) return TV_ERR_SHAPE;
+    if (!argmax_args_ok(B, N, V)) return TV_ERR_SHAPE;
     if (B == 0) return TV_OK;
-    if (!logits || !draft_tokens || !parent || !argmax_out || !accept_len || !accept_idx ||
-        !bonus_token || !workspace)
+    if (!argmax_ptrs_ok(logits, draft_tokens, parent, argmax_out, accept_len, accept_idx,
+                        bonus_token) || !workspace)
         return TV_ERR_NULL;
     if ((reinterpret_cast<uintptr_t>(logits) & 3u) || (reinterpret_cast<uintptr_t>(workspace) & 7u))
         return TV_ERR_ALIGN;
     if (workspace_bytes < tv_argmax_workspace_size(B, N, V)) return TV_ERR_WORKSPACE;
     if (!device_ok()) return TV_ERR_DEVICE;
-    int segs = 1, seg_len = 4;
-    argmax_plan(B, N, V, &segs, &seg_len);
-    const hipError_t e = tv::launch_argmax_accept(
-        logits, draft_tokens, parent, num_nodes, B, N, V, segs, seg_len, argmax_out, accept_len,
-        accept_idx,
-        bonus_token, static_cast<unsigned long long *>(workspace), stream);
-    return e == hipSuccess ? TV_OK : TV_ERR_HIP;
+    return argmax_accept_checked(logits, draft_tokens, parent, num_nodes, B, N, V, argmax_out,
+                                 accept_len, accept_idx, bonus_token, workspace, stream);
+}
+
+int tree_argmax_accept_noalloc(const float *logits, const int32_t *draft_tokens,
+                               const int32_t *parent, const int32_t *num_nodes, int B, int N,
+                               int V, int32_t *argmax_out, int32_t *accept_len,
+                               int32_t *accept_idx, int32_t *bonus_token, hipStream_t stream) {
+    if (!argmax_args_ok(B, N, V)) return TV_ERR_SHAPE;
+    if (B == 0) return TV_OK;
+    if (!argmax_ptrs_ok(logits, draft_tokens, parent, argmax_out, accept_len, accept_idx,
+                        bonus_token))
+        return TV_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(logits) & 3u) return TV_ERR_ALIGN;
+    if (tv_argmax_workspace_size(B, N, V) > (size_t)TV_NOALLOC_SCRATCH_BYTES)
+        return TV_ERR_SCRATCH;
+    if (!device_ok()) return TV_ERR_DEVICE;
+    void *ws = scratch_ptr();
+    if (ws == nullptr) return TV_ERR_HIP;
+    return argmax_accept_checked(logits, draft_tokens, parent, num_nodes, B, N, V, argmax_out,
+                                 accept_len, accept_idx, bonus_token, ws, stream);
 }
 
 int kv_compact_accepted(const uint16_t *k_tree, const uint16_t *v_tree, uint16_t *k_cache,

@@ -47,8 +47,8 @@ def test_only_declared_symbols_are_exported():
 
 
 def test_status_strings(lib):
-    assert lib.tv_abi_version() == 4
-    for code in range(0, -7, -1):
+    assert lib.tv_abi_version() == 5
+    for code in range(0, -8, -1):
         assert lib.tv_status_string(code)
     assert lib.tv_status_string(-99) == b"unknown status"
 
@@ -104,6 +104,18 @@ def test_accept_and_compact_argument_checks(lib):
     assert acc(N=300) == -2 and acc(V=0) == -2
     assert acc(wsb=8) == -4
     assert acc(l=ctypes.c_void_p(0x10002)) == -3
+    noalloc = lambda **kw: lib.tree_argmax_accept_noalloc(
+        *{**dict(l=FAKE, d=FAKE, p=FAKE, nn=NULL, B=2, N=4, V=100, a=FAKE, al=FAKE, ai=FAKE,
+                 b=FAKE), **kw}.values(), STREAM)
+    assert noalloc(B=0) == 0
+    assert noalloc(l=NULL) == -1 and noalloc(b=NULL) == -1
+    assert noalloc(N=300) == -2 and noalloc(V=0) == -2
+    assert noalloc(l=ctypes.c_void_p(0x10002)) == -3
+    # the static scratch holds 4 MiB of segment keys: 524256 node rows at most
+    assert lib.tv_argmax_workspace_size(2047, 256, 128256) <= 4 << 20 < \
+        lib.tv_argmax_workspace_size(2048, 256, 128256)
+    assert noalloc(B=2048, N=256, V=128256) == -7
+    assert noalloc(B=2047, N=256, V=128256) in (-6, -5)   # fits; no gfx950 here
     cmp_ = lambda **kw: lib.kv_compact_accepted(*{**dict(kt=FAKE, vt=FAKE, kc=FAKE, vc=FAKE,
                                                           pt=FAKE, kl=FAKE, ai=FAKE, al=FAKE,
                                                           B=2, N=4, Hkv=8, D=128, P=16, mp=4,
