@@ -34,10 +34,11 @@ def _run(cmd):
 def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
     """Compile every source to an object in parallel, then link the shared
     library; the result replaces `out` only when every step succeeded."""
+    import shutil
+    import tempfile
     from concurrent.futures import ThreadPoolExecutor
-    tag = "%d" % os.getpid()
-    objs = [os.path.join(HERE, "csrc", os.path.basename(src)[:-4] + f".{tag}.o")
-            for src in sources()]
+    tmpdir = tempfile.mkdtemp(prefix="treeverify_build_")
+    objs = [os.path.join(tmpdir, os.path.basename(src)[:-4] + ".o") for src in sources()]
     cmds = [[HIPCC, *FLAGS, *extra_flags, "-c", src, "-o", obj]
             for src, obj in zip(sources(), objs)]
     try:
@@ -50,15 +51,15 @@ def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
                 raise RuntimeError(f"hipcc failed on {cmd[-3]}:\n" + err)
             if verbose and err.strip():
                 print(err, file=sys.stderr)
-        tmp = out + ".tmp" + tag
+        tmp = os.path.join(tmpdir, "lib.so")
         rc, err = _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
         if rc != 0:
             raise RuntimeError("link failed:\n" + err)
-        os.replace(tmp, out)
+        shutil.copyfile(tmp, out + ".part")
+        os.chmod(out + ".part", 0o755)
+        os.replace(out + ".part", out)
     finally:
-        for obj in objs:
-            if os.path.exists(obj):
-                os.remove(obj)
+        shutil.rmtree(tmpdir, ignore_errors=True)
     return out
 
 

@@ -19,19 +19,26 @@
 //     output in bf16) that a second kernel merges with the usual log-sum-exp
 //     rescaling.
 //   * K and V tiles stream from HBM straight into a 4-stage LDS ring with
-//     global_load_lds_dwordx4 (no register staging), two tiles ahead of the
-//     one being computed. Each 256-byte row is stored with its 16-byte chunks
-//     XOR-swizzled by the key index, so the MFMA operand reads below are free
-//     of bank conflicts. Keys past the prefix, and tree slots past N, load a
-//     harmless finite row (tree node 0) and are masked; the NaN-filled tail
-//     slots of a cache page are never read.
-//   * Each wave owns 32 query rows. Per 32-key half tile it computes
-//     S^T = K * Q^T with v_mfma_f32_32x32x16_bf16 (keys on M, rows on N: a lane
-//     holds 16 scores of one row, so a row max/sum needs one cross-half
-//     exchange), masks, runs the online softmax in fp32 (base-2 exponent with
-//     the scale folded into one FMA), and accumulates O^T = V^T * P^T with the
-//     same instruction. V^T operands come from the row-major tile through
-//     ds_read_b64_tr_b16, which transposes 4x16 blocks on the way out of LDS.
+//     global_load_lds_dwordx4 (no register staging). Each 256-byte row is
+//     stored with its 16-byte chunks XOR-swizzled by the key index, so the
+//     MFMA operand reads below are free of bank conflicts. Keys past the
+//     prefix, and tree slots past N, load a harmless finite row (tree node 0)
+//     and are masked; the NaN-filled tail slots of a cache page are never read.
+//   * Each wave owns 32 query rows; the workgroup's 8 waves step through the
+//     tiles together, one workgroup barrier per 64-key tile ("period"). In
+//     period j every wave computes S^T = K_j Q^T with
+//     v_mfma_f32_32x32x16_bf16 (keys on M, rows on N: a lane holds 16 scores
+//     of one row, so a row max/sum needs one cross-half exchange) and
+//     O^T += V_{j-1}^T P_{j-1}^T with the same instruction, and puts the
+//     softmax work (mask, max, fp32 exponentials in base 2 with the scale
+//     folded into one FMA, bf16 P^T) between those MFMAs, so that one wave's
+//     matrix and vector work overlap. V^T operands come from the row-major
+//     tile through ds_read_b64_tr_b16, which transposes 4x16 blocks on the
+//     way out of LDS.
+//   * At the end of period j each wave issues its share of K_{j+3} and
+//     V_{j+2} in one burst: DMA writes into LDS slow down every wave's operand
+//     reads, and a single burst per period disturbs them least. Each load is
+//     issued about three periods before it is read.
 //   * Reads of the ring are inline assembly with explicit lgkmcnt waits tied to
 //     the fragments they produce, and ring hand-off is s_waitcnt vmcnt(n) +
 //     s_barrier, so the compiler never inserts a blanket wait for the
@@ -172,18 +179,6 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit field");
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-__device__ __forceinline__ void wait_tile_loads(int newer_tiles, int loads_per_tile) {
-    // At most newer_tiles * loads_per_tile later loads may stay in flight; a
-    // count without its own case waits for the next smaller one (stricter).
-    const int n = newer_tiles * loads_per_tile;
-    if (n >= 32) wait_vmcnt<32>();
-    else if (n >= 16) wait_vmcnt<16>();
-    else if (n >= 8) wait_vmcnt<8>();
-    else if (n >= 4) wait_vmcnt<4>();
-    else if (n >= 2) wait_vmcnt<2>();
-    else wait_vmcnt<0>();
 }
 
 // Exclusive prefix sum of per-sequence tile counts into g_cum[0..B], the
@@ -350,6 +345,7 @@ struct TileIssue {
     int kib;                                          // this lane's key within a block
     unsigned row_off;                                 // kib * key row stride (bytes)
     unsigned chunk_off[LPT];                          // swizzled chunk offset per load
+    unsigned lane_off[LPT];                           // i * KPB rows + row_off + chunk_off[i]
     // per unit
     const char *kc_g, *vc_g;                          // cache base + KV head g
     const char *kt_g, *vt_g;                          // tree row of node 0, KV head g
@@ -365,7 +361,34 @@ struct TileIssue {
         for (int i = 0; i < LPT; ++i) {
             const int kb = wave_u * LPT + i;
             chunk_off[i] = (unsigned)(((lane % C) ^ swz<C>((kb * KPB + kib) % C)) * 16);
+            lane_off[i] = (unsigned)(i * KPB) * row_bytes + row_off + chunk_off[i];
         }
+    }
+
+    // Common case of a prefix tile: every row of the tile exists, this wave's
+    // LPT blocks (consecutive keys) lie in one page, and that page id (pg0,
+    // the page of the wave's first key) is valid. Then block i starts
+    // i * KPB rows after `off`, the byte offset of the wave's first key row
+    // from the cache base of KV head g. Returns false otherwise.
+    __device__ __forceinline__ bool fast_offset(const AttnParams &p, int t, int wave_u, int pg0,
+                                                unsigned long long &off) const {
+        const int pos_w = t * KT + wave_u * LPT * KPB;
+        if (LPT * KPB > p.P || t >= ntp || t * KT + KT > L || (unsigned)pg0 >= (unsigned)p.num_pages)
+            return false;
+        off = (unsigned long long)(unsigned)pg0 * page_bytes + (unsigned)(pos_w & (p.P - 1)) * row_bytes;
+        return true;
+    }
+
+    // Direct-to-LDS loads of this wave's blocks of one K (or V) tile of the
+    // common case (see fast_offset) into ring stage `stage`.
+    __device__ __forceinline__ void issue_fast(unsigned long long off, bool is_v, int stage,
+                                               int wave_u) const {
+        unsigned char *dst = g_ring + stage * Gm::kStageBytes + (is_v ? Gm::kTileBytes : 0);
+        const char *base = (is_v ? vc_g : kc_g) + off;
+        #pragma unroll
+        for (int i = 0; i < LPT; ++i)
+            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(base + lane_off[i]),
+                                             (LDS_AS void *)(dst + (wave_u * LPT + i) * 1024), 16, 0, 0);
     }
 
     __device__ __forceinline__ void set_unit(const AttnParams &p, int b, int g, int L_, int ntp_,
@@ -428,16 +451,6 @@ struct TileIssue {
             }
         }
         return r;
-    }
-
-    // Direct-to-LDS load of block i of this wave's share of one K (or V) tile
-    // into ring stage `stage`.
-    __device__ __forceinline__ void issue_one(const Blocks &bl, bool is_v, int stage, int wave_u,
-                                              int i) const {
-        unsigned char *dst = g_ring + stage * Gm::kStageBytes + (is_v ? Gm::kTileBytes : 0);
-        const char *addr = (is_v ? bl.v[i] : bl.k[i]) + ((kib < bl.nv[i] ? row_off : 0u) + chunk_off[i]);
-        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)addr,
-                                         (LDS_AS void *)(dst + (wave_u * LPT + i) * 1024), 16, 0, 0);
     }
 
     // Direct-to-LDS loads of this wave's blocks of one K (or V) tile into ring
@@ -505,185 +518,196 @@ __device__ __forceinline__ void lds_wait_n(int n) {
     }
 }
 
-// Per-wave state of one segment: Q fragments (MFMA B operand), O^T
-// accumulators, the current tile's scores and probabilities, running max/sum.
+// Per-wave state of one piece: Q fragments (MFMA B operand), O^T
+// accumulators, the probabilities of the tile whose PV product is pending,
+// running max and sum.
 template <int D>
 struct WaveState {
     static constexpr int NKS = D / 16;     // MFMA k-steps over the head dim
     static constexpr int NDT = D / 32;     // 32-wide head-dim tiles of the output
     bf16x8 qf[NKS];
     f32x16 o[NDT];
-    f32x16 s[2];                           // S^T of the 2 x 32 keys of the tile
-    bf16x8 pb[4];                          // P^T, 16 keys per k-step
+    u32x4 pb[4];                           // P^T as bf16 pairs, 16 keys per k-step
     float m_run;                           // running max (raw score units)
+    float msc;                             // m_run * scale_log2 (0 while m_run is -inf)
     float l_run;                           // this lane's part of the running sum
 };
 
-// Matrix phase of one wave: O^T += V^T P^T for the previous tile (PV) and
-// S^T = K Q^T for the current tile (SC). The ring reads are issued two
-// groups ahead of the MFMAs that consume them; groups alternate PV / S so
-// that consecutive MFMAs rarely depend on each other. hook(g) runs after
-// group g: the caller issues its global->LDS tile loads there, a few at a
-// time, instead of in one burst that would stall the wave.
-template <int D, bool PV, bool SC, typename Hook>
-__device__ __forceinline__ void matrix_phase(WaveState<D> &st, unsigned kaddr, unsigned vaddr,
-                                             Hook &&hook) {
-    using Gm = Geo<D>;
-    constexpr int NKS = D / 16, NDT = D / 32, KH = NKS / 2;
-    constexpr int C = Gm::kChunks;
-    // group g: even g = PV k-step g/2, odd g = S quarter g/2 (half q/2, k-range q%2)
-    constexpr int kGroups = 8;
-    auto active = [](int gi) { return (gi & 1) ? SC : PV; };
-    auto reads_of = [](int gi) { return (gi & 1) ? KH : 2 * NDT; };
-    u32x2 vb[4][NDT][2];
-    u32x4 kb[4][KH];
-    auto issue = [&](int gi) {
-        if (gi & 1) {
-            const int q = gi >> 1, hf = q >> 1, part = q & 1;
-            #pragma unroll
-            for (int i = 0; i < KH; ++i) {
-                const int ks = part * KH + i;
-                asm volatile("ds_read_b128 %0, %1 offset:%2"
-                             : "=v"(kb[q][i])
-                             : "v"(kaddr ^ ((unsigned)ks << 5)), "i"(hf * 32 * Gm::kRowBytes));
-            }
-        } else {
-            const int kk = gi >> 1;
-            #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-                #pragma unroll
-                for (int rr = 0; rr < 2; ++rr) {
-                    const unsigned flip = (unsigned)((dt * 4) ^ swz<C>((rr * 8) % C)) << 4;
-                    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
-                                 : "=v"(vb[kk][dt][rr])
-                                 : "v"(vaddr ^ flip), "i"((kk * 16 + rr * 8) * Gm::kRowBytes));
-                }
-        }
-    };
-    auto consume = [&](int gi) {
-        if (gi & 1) {
-            const int q = gi >> 1, hf = q >> 1, part = q & 1;
-            #pragma unroll
-            for (int i = 0; i < KH; ++i) {
-                tie(kb[q][i]);
-                st.s[hf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8, kb[q][i]), st.qf[part * KH + i], st.s[hf], 0, 0, 0);
-            }
-        } else {
-            const int kk = gi >> 1;
-            #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                tie(vb[kk][dt][0]);
-                tie(vb[kk][dt][1]);
-                const u32x4 a = {vb[kk][dt][0][0], vb[kk][dt][0][1], vb[kk][dt][1][0], vb[kk][dt][1][1]};
-                st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8, a), st.pb[kk], st.o[dt], 0, 0, 0);
-            }
-        }
-    };
-    if (SC) {
-        #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-            #pragma unroll
-            for (int r = 0; r < 16; ++r) st.s[hf][r] = 0.f;
-    }
-    // active groups in order; next(gi) = following active group (or kGroups)
-    auto next = [&](int gi) {
-        int n = gi + 1;
-        while (n < kGroups && !active(n)) ++n;
-        return n;
-    };
-    const int g0 = next(-1);
-    const int g1 = next(g0);
-    issue(g0);
-    if (g1 < kGroups) issue(g1);
-    #pragma unroll
-    for (int gi = 0; gi < kGroups; ++gi) {
-        if (active(gi)) {
-            const int gn = next(gi);
-            lds_wait_n(gn < kGroups ? reads_of(gn) : 0);
-            consume(gi);
-            const int gnn = gn < kGroups ? next(gn) : kGroups;
-            if (gnn < kGroups) issue(gnn);
-        }
-        hook(gi);          // the caller's tile loads, spread over the phase
-    }
+// Visible keys of tile j for the lane's row: every key of a full prefix tile
+// (masked = false, wave-uniform), the keys below the prefix length on the last
+// prefix tile, the node's ancestors on a tree tile. Bit k of (vis_hi:vis_lo)
+// is the key the lane holds at position k of a half-0 lane (the lane's own
+// half already shifted in).
+struct TileMask {
+    bool masked;
+    unsigned vis_lo, vis_hi;
+};
+
+// Key position (within the tile) of accumulator element r of half hf, for a
+// lane of half 0; a lane of half 1 holds the key 4 positions later.
+__host__ __device__ constexpr int key_of(int hf, int r) { return hf * 32 + (r >> 2) * 8 + (r & 3); }
+
+// Exponentials of 2 scores of one tile into a bf16 pair of P^T and the
+// running sum: x = 2^(s * c - msc).
+// The results are tied (empty volatile asm) so that the computation stays in
+// the MFMA slot it was written in instead of sinking to its first use.
+__device__ __forceinline__ unsigned exp_pair(float s0, float s1, float c, float msc, float &sum) {
+    const float x0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s0, c, -msc));
+    const float x1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s1, c, -msc));
+    sum += x0 + x1;
+    const bf16x2 pr = {(__bf16)x0, (__bf16)x1};
+    unsigned u = __builtin_bit_cast(unsigned, pr);
+    tie(u);
+    tie(sum);
+    return u;
 }
 
-// Softmax phase of one wave for tile t: mask, tile max, lazy rescale of the
-// running state, exponentials into P^T (bf16) and the running sum.
-template <int D>
-__device__ __forceinline__ void softmax_phase(WaveState<D> &st, const AttnParams &p, int t,
-                                              int ntp, int L, int node, int half) {
-    constexpr int NDT = D / 32;
-    // Lane holds keys hf*32 + (r/4)*8 + half*4 + r%4 of its row.
-    if (t < ntp) {
-        const int lim_t = L - t * KT;                   // keys >= lim_t are past the prefix
-        if (lim_t < KT) {                               // wave-uniform: only the last prefix tile
-            const int lim = lim_t - half * 4;
+// One tile period of one wave.
+//   CUR:  part A computes tile j's scores S^T = K_j Q^T into s0 (keys 0..31)
+//         and s1 (keys 32..63); part B masks them, takes their maximum,
+//         decides the running maximum and exponentiates half 0 into P^T.
+//   PREV: the first half of part A exponentiates the previous tile's half 1
+//         (in s1, consumed before this tile's half-1 products overwrite it);
+//         part B adds P^T V_{j-1} to O.
+// The VALU slices sit between the MFMAs of their part, so the matrix pipe and
+// the VALU of one wave overlap; two 16-register score halves are alive at any
+// time. LDS operand reads run two MFMAs ahead with explicit waits.
+template <int D, bool PREV, bool CUR>
+__device__ __forceinline__ void tile_period(WaveState<D> &st, f32x16 &sc0, f32x16 &sc1,
+                                            unsigned kaddr, unsigned vaddr, const TileMask &mk,
+                                            float c) {
+    f32x16 *sc[2] = {&sc0, &sc1};
+    using Gm = Geo<D>;
+    constexpr int NKS = D / 16, NDT = D / 32;
+    constexpr int C = Gm::kChunks;
+    constexpr int SA = 2 * NKS;            // part A slots: one S MFMA each
+    constexpr int SB = 4 * NDT;            // part B slots: one PV MFMA each
+    constexpr int NSLOT = SA + SB;
+    constexpr int R = 2;                   // operand reads run this many slots ahead
+    constexpr int PPA = 8 / NKS;                       // half-1 pairs per slot of part A's first half
+    // first part-B slot of the half-0 pairs: after the decision (slot 5) and
+    // after the PV MFMAs that read P^T k-steps 0 and 1 have issued
+    constexpr int B0 = 2 * NDT > 6 ? 2 * NDT : 6;
+    constexpr int PPB = (8 + (SB - B0) - 1) / (SB - B0);   // half-0 pairs per part-B slot
+    static_assert(NKS <= 8 && 8 % NKS == 0 && SB > B0, "slice shapes");
+    auto active = [](int s) { return s < SA ? CUR : PREV; };
+    auto ops = [&](int s) { return (s < NSLOT && active(s)) ? (s < SA ? 1 : 2) : 0; };
+    u32x4 kb[SA];
+    u32x2 vb[SB][2];
+    auto issue_reads = [&](int s) {
+        if (s >= NSLOT || !active(s)) return;
+        if (s < SA) {
+            const int hf = s / NKS, ks = s % NKS;
+            asm volatile("ds_read_b128 %0, %1 offset:%2"
+                         : "=v"(kb[s])
+                         : "v"(kaddr ^ ((unsigned)ks << 5)), "i"(hf * 32 * Gm::kRowBytes));
+        } else {
+            const int b = s - SA, kk = b / NDT, dt = b % NDT;
+            #pragma unroll
+            for (int rr = 0; rr < 2; ++rr) {
+                const unsigned flip = (unsigned)((dt * 4) ^ swz<C>((rr * 8) % C)) << 4;
+                asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                             : "=v"(vb[b][rr])
+                             : "v"(vaddr ^ flip), "i"((kk * 16 + rr * 8) * Gm::kRowBytes));
+            }
+        }
+    };
+    float psa = 0.f, psb = 0.f;
+    float m8[4];
+    float alpha = 1.f;
+    bool any_raise = false;
+    #pragma unroll
+    for (int s = 0; s < R; ++s) issue_reads(s);
+    #pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+        issue_reads(s + R);
+        if (active(s)) {
+            int newer = 0;
+            #pragma unroll
+            for (int k = 1; k <= R; ++k) newer += ops(s + k);
+            lds_wait_n(newer);
+            if (s < SA) {
+                const int hf = s / NKS, ks = s % NKS;
+                tie(kb[s]);
+                const f32x16 acc = ks == 0 ? f32x16{} : *sc[hf];   // a chain starts from zero
+                *sc[hf] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kb[s]),
+                                                                  st.qf[ks], acc, 0, 0, 0);
+            } else {
+                const int b = s - SA, kk = b / NDT, dt = b % NDT;
+                tie(vb[b][0]);
+                tie(vb[b][1]);
+                const u32x4 a = {vb[b][0][0], vb[b][0][1], vb[b][1][0], vb[b][1][1]};
+                st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, st.pb[kk]), st.o[dt],
+                    0, 0, 0);
+            }
+        }
+        if (PREV && s < NKS) {
+            // pairs of the previous tile's half 1 (keys 32 + 2i, 33 + 2i: P^T
+            // k-steps 2, 3), all before slot NKS overwrites s1
+            #pragma unroll
+            for (int u = 0; u < PPA; ++u) {
+                const int i = s * PPA + u, kk = 2 + (i >> 2), w = i & 3;
+                st.pb[kk][w] = exp_pair(sc1[2 * i], sc1[2 * i + 1], c, st.msc, psa);
+            }
+        }
+        if (PREV && s == NKS - 1) st.l_run += psa;
+        if (CUR && s == SA + 1 && mk.masked) {
+            // the last prefix tile or a tree tile: invisible keys become -inf
+            // (selected, never added), in place
             #pragma unroll
             for (int hf = 0; hf < 2; ++hf)
                 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    st.s[hf][r] = (hf * 32 + (r >> 2) * 8 + (r & 3) >= lim) ? kNegInf : st.s[hf][r];
+                for (int r = 0; r < 16; ++r) {
+                    const int k = key_of(hf, r);
+                    const unsigned word = k < 32 ? mk.vis_lo : mk.vis_hi;
+                    (*sc[hf])[r] = ((word >> (k & 31)) & 1u) ? (*sc[hf])[r] : kNegInf;
+                }
         }
-    } else {
-        const unsigned long long vis = g_anc[node][t - ntp] >> (half * 4);
-        #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-            #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                st.s[hf][r] = ((vis >> (hf * 32 + (r >> 2) * 8 + (r & 3))) & 1ull) ? st.s[hf][r] : kNegInf;
-    }
-    // The running max is only raised when a score exceeds it by more than
-    // kRescaleSlack (log2 units), so O is rarely rescaled. The tile max is a
-    // tree of three-input maxes.
-    float v[32];
-    #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        v[r] = st.s[0][r];
-        v[16 + r] = st.s[1][r];
-    }
-    float m1[12];
-    #pragma unroll
-    for (int i = 0; i < 10; ++i) m1[i] = max3(v[3 * i], v[3 * i + 1], v[3 * i + 2]);
-    m1[10] = v[30];
-    m1[11] = v[31];
-    const float m2a = max3(m1[0], m1[1], m1[2]), m2b = max3(m1[3], m1[4], m1[5]);
-    const float m2c = max3(m1[6], m1[7], m1[8]), m2d = max3(m1[9], m1[10], m1[11]);
-    const float tmax = halves_max(max3(m2a, m2b, fmaxf(m2c, m2d)));
-    const bool raise = tmax * p.scale_log2 > st.m_run * p.scale_log2 + kRescaleSlack;
-    if (__any(raise)) {
-        const float m_new = raise ? tmax : st.m_run;
-        const float alpha = (st.m_run == kNegInf) ? 0.f
-                            : __builtin_amdgcn_exp2f((st.m_run - m_new) * p.scale_log2);
-        st.l_run *= alpha;
-        #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-            #pragma unroll
-            for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
-        st.m_run = m_new;
-    }
-    const float msc = (st.m_run == kNegInf) ? 0.f : st.m_run * p.scale_log2;
-    float ps[4] = {0.f, 0.f, 0.f, 0.f};
-    #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-        #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const float x = __builtin_amdgcn_exp2f(
-                __builtin_fmaf(st.s[kk >> 1][(kk & 1) * 8 + e], p.scale_log2, -msc));
-            ps[e & 3] += x;
-            st.pb[kk][e] = (__bf16)x;
+        if (CUR && s >= SA + 1 && s < SA + 5) {
+            // maximum of 8 of this tile's scores (chunk q: half q / 2, elements
+            // 8 (q % 2) .. +8)
+            const int q = s - SA - 1, hf = q >> 1, r0 = (q & 1) * 8;
+            const f32x16 &v = *sc[hf];
+            const float a = max3(v[r0], v[r0 + 1], v[r0 + 2]);
+            const float b = max3(v[r0 + 3], v[r0 + 4], v[r0 + 5]);
+            m8[q] = max3(a, b, max3(v[r0 + 6], v[r0 + 7], v[r0 + 7]));
+            tie(m8[q]);
         }
-    st.l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
-}
-
-// Barrier between the phases of the two wave groups; nothing is scheduled
-// across it.
-__device__ __forceinline__ void phase_barrier() {
-    __builtin_amdgcn_sched_barrier(0);
-    lds_barrier();
-    __builtin_amdgcn_sched_barrier(0);
+        if (CUR && s == SA + 5) {
+            // The running max is only raised when a score exceeds it by more
+            // than kRescaleSlack (log2 units), so O is rarely rescaled. The
+            // sum is rescaled here; O after this period's PV products.
+            const float tmax = halves_max(max3(m8[0], m8[1], max3(m8[2], m8[3], m8[3])));
+            const bool raise = tmax * c > st.m_run * c + kRescaleSlack;
+            any_raise = __any(raise);
+            if (any_raise) {
+                const float m_new = raise ? tmax : st.m_run;
+                alpha = (st.m_run == kNegInf) ? 0.f
+                        : __builtin_amdgcn_exp2f((st.m_run - m_new) * c);
+                st.l_run *= alpha;
+                st.m_run = m_new;
+            }
+            st.msc = (st.m_run == kNegInf) ? 0.f : st.m_run * c;
+        }
+        if (CUR && s >= SA + B0) {
+            #pragma unroll
+            for (int u = 0; u < PPB; ++u) {
+                const int i = (s - SA - B0) * PPB + u;     // pair i of half 0: keys 2i, 2i + 1
+                if (i < 8) st.pb[i >> 2][i & 3] = exp_pair(sc0[2 * i], sc0[2 * i + 1], c, st.msc, psb);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (CUR) {
+        st.l_run += psb;
+        if (any_raise) {
+            #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+                #pragma unroll
+                for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
+        }
+    }
 }
 
 template <int D, int NW, bool SMALL>
@@ -698,10 +722,6 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave_u = __builtin_amdgcn_readfirstlane(tid / kWave);
-    // Two wave groups run half a tile apart: while one group is in its matrix
-    // phase the other is in its softmax phase, so every SIMD has MFMA and VALU
-    // work from different waves at the same time.
-    const int grp = (NW >= 2 && wave_u >= NW / 2) ? 1 : 0;
     const int half = lane >> 5;
     const int col = lane & 31;
     const int w = xcd_contiguous_id(blockIdx.x, p.num_wg);
@@ -794,6 +814,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             #pragma unroll
             for (int r = 0; r < 16; ++r) st.o[dt][r] = 0.f;
         st.m_run = kNegInf;
+        st.msc = 0.f;
         st.l_run = 0.f;
 
         const int npages = (L + p.P - 1) >> p.p_shift;
@@ -802,6 +823,9 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         auto vaddr_of = [&](int t) {
             return ring_base + (t & (NS - 1)) * Gm::kStageBytes + Gm::kTileBytes + v_lane;
         };
+        // Scores of the current tile: half 0 in s0, half 1 in s1 (exponentiated
+        // early in the next period).
+        f32x16 s0, s1;
 
         // The segment runs in sub-ranges whose prefix pages fit the LDS page-id
         // window (one sub-range unless a piece spans more than kPageCache pages).
@@ -820,58 +844,51 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             if (SMALL && ta < ntp) load_pages<NT>(p, b, page_first, npages);
 
             const int T = tb - ta;
-            // Load batch i = K tile ta+i and V tile ta+i-1 (those that exist). It is
-            // issued two tile periods before the matrix phase that first needs it
-            // (a third period ahead measured 2 % slower: the extra loads in flight
-            // only lengthen the issue stalls).
-            auto batch_loads = [&](int i) {
-                return ((i >= 0 && i < T) ? LPT : 0) + ((i >= 1 && i <= T) ? LPT : 0);
+            // Tile i of the sub-range (K and V of tile ta + i) goes to ring stage
+            // (ta + i) % NS. Period j computes S with K_j and PV with V_{j-1}, and
+            // issues K_{j+3} and V_{j+2}: the K half it refills last held K_{j-1}
+            // (read in period j - 1), the V half V_{j-2} (read in period j - 1),
+            // both before the barrier that opens period j. Every load is issued
+            // about three periods before it is read.
+            int pk[LPT];                       // page ids of the next K tile to be loaded
+            typename Issue::Blocks bk;         // block addresses of the last K tile issued,
+            bool fast = false;                 // or, when `fast`, its common-case offset
+            unsigned long long foff = 0;
+            auto blocks_of = [&](int i) { return ld.blocks(p, ta + i, wave_u, pk); };
+            auto issue_half = [&](int i, bool is_v, const typename Issue::Blocks &bl) {
+                const int t = ta + i;
+                if (SMALL && t < ntp) ld.issue_small(p, t, is_v, page_first, wave_u);
+                else ld.issue(bl, is_v, t & (NS - 1), wave_u);
             };
-            // pk: page ids of the K tile of the next batch (fetched one tile
-            // period ahead); last: blocks of the last issued K tile, which is
-            // the V tile of the next batch.
-            int pk[LPT];
-            typename Issue::Blocks last;
-            auto issue_batch = [&](int i) {
-                const int tk = ta + i, tv = ta + i - 1;
-                if (SMALL) {
-                    if (i < T) {
-                        if (tk < ntp) ld.issue_small(p, tk, false, page_first, wave_u);
-                        else ld.issue(ld.blocks(p, tk, wave_u, pk), false, tk & (NS - 1), wave_u);
-                    }
-                    if (i >= 1 && i <= T) {
-                        if (tv < ntp) ld.issue_small(p, tv, true, page_first, wave_u);
-                        else ld.issue(ld.blocks(p, tv, wave_u, pk), true, tv & (NS - 1), wave_u);
-                    }
-                    return;
-                }
-                typename Issue::Blocks cur;
-                if (i < T) {
-                    cur = ld.blocks(p, tk, wave_u, pk);
-                    ld.issue(cur, false, tk & (NS - 1), wave_u);
-                }
-                if (i >= 1 && i <= T) ld.issue(last, true, tv & (NS - 1), wave_u);
-                last = cur;
-            };
-            auto fetch = [&](int i) { ld.fetch_pages(p, b, ta + i, wave_u, pk); };
-
-            // Q (issued above) and the first tiles are in flight together: the
-            // first tile wait below also covers Q, which was issued earlier.
             ld.set_unit(p, b, g, L, ntp, nodes);
             {
-                int ids[3][LPT];
+                int ids[4][LPT];
                 #pragma unroll
-                for (int i = 0; i < 3; ++i) ld.fetch_pages(p, b, ta + i, wave_u, ids[i]);
+                for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, ta + i, wave_u, ids[i]);
+                typename Issue::Blocks b0, b1;
                 #pragma unroll
-                for (int i = 0; i < 3; ++i) {
-                    #pragma unroll
-                    for (int k = 0; k < LPT; ++k) pk[k] = ids[i][k];
-                    if (i < 2) issue_batch(i);    // pk then holds the ids of batch 2
+                for (int k = 0; k < LPT; ++k) pk[k] = ids[0][k];
+                b0 = blocks_of(0);
+                #pragma unroll
+                for (int k = 0; k < LPT; ++k) pk[k] = ids[1][k];
+                b1 = blocks_of(1);
+                #pragma unroll
+                for (int k = 0; k < LPT; ++k) pk[k] = ids[2][k];
+                bk = blocks_of(2);             // K_2 now, V_2 in period 0
+                // issue order K_0, V_0, K_1, V_1, K_2 (the waits below count on it)
+                issue_half(0, false, b0);
+                issue_half(0, true, b0);
+                if (T > 1) {
+                    issue_half(1, false, b1);
+                    issue_half(1, true, b1);
                 }
+                if (T > 2) issue_half(2, false, bk);
+                #pragma unroll
+                for (int k = 0; k < LPT; ++k) pk[k] = ids[3][k];
             }
-            // Ancestor sets, while the loads above are in flight, by one wave
-            // (the other waves only read them at the tree tiles, after several
-            // workgroup barriers): in registers up to 64 nodes, else in LDS.
+            // Ancestor sets, while the first loads are in flight, by one wave (the
+            // others read them only after the next workgroup barrier): in
+            // registers up to 64 nodes, else in LDS.
             if (want_anc) {
                 if (wave_u == 0) {
                     if (p.N <= kWave) build_ancestor_masks_wave(p, b);
@@ -880,100 +897,80 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                 anc_b = b;
             }
 
-            // Slots of half a tile period, separated by workgroup barriers. Group 0
-            // runs matrix j in slot 2j and softmax j in slot 2j+1; group 1 runs
-            // the same instruction stream one slot later (one extra barrier at
-            // its start, one at group 0's end). Batch j must have landed, for
-            // every wave, before slot 2j: group 0 waits before the barrier that
-            // opens its matrix j, group 1 before the one that opens its softmax
-            // j-1. Both groups issue batch j+2 when they start matrix j; the
-            // ring stages it overwrites were last read in slot 2j-3.
-            if (grp == 1) {
-                wait_vm_at_most(batch_loads(1));
-                phase_barrier();
-            }
-            // slot pair j: barrier, matrix j (issuing batch j+2 along the way);
-            // barrier, softmax j
-            typename Issue::Blocks cur;
-            bool have_k = false, have_v = false;
-            int stage_k = 0, stage_v = 0;
-            // Waits: batch j (group 0, before matrix j) or batch j+1 (group 1,
-            // before softmax j) complete, leaving this wave's loads of the one
-            // later batch in flight.
-            auto open_matrix = [&](int j) {
-                if (grp == 0) wait_vm_at_most(batch_loads(j + 1));
-                phase_barrier();
-                // The matrix phase runs at raised wave priority: when both waves of
-                // a SIMD could issue, its MFMAs and LDS reads go first and the other
-                // group's softmax fills the gaps.
-                __builtin_amdgcn_s_setprio(1);
-                const int i = j + 2;
-                have_k = have_v = false;
-                if (i <= T) {
-                    if (SMALL) {
-                        issue_batch(i);
+            // Loads this wave issues at the end of period i (V_{i+2}, K_{i+3} when they exist).
+            auto loads_in = [&](int i) { return (i + 3 < T ? LPT : 0) + (i + 2 < T ? LPT : 0); };
+            // Opening of period j: K_j and V_{j-1} have landed for every wave (this
+            // wave's later loads may still be in flight) and every wave is done
+            // with period j - 1; then tile j's mask.
+            TileMask mk;
+            auto open_period = [&](int j) {
+                int newer;                     // loads issued after the last one period j needs
+                if (j == 0) newer = LPT * ((T > 1 ? 2 : 0) + (T > 2 ? 1 : 0)) + LPT;   // V_0, K_1, V_1, K_2
+                else if (j == 1) newer = LPT * ((T > 1 ? 1 : 0) + (T > 2 ? 1 : 0)) + loads_in(0);
+                else if (j == 2) newer = loads_in(0) + loads_in(1);
+                else newer = loads_in(j - 2) + loads_in(j - 1);
+                wait_vm_at_most(newer);
+                lds_barrier();
+                const int t = ta + j;
+                unsigned long long vis;
+                if (t < ntp) {
+                    const int lim_t = L - t * KT;      // keys at or past it lie beyond the prefix
+                    mk.masked = lim_t < KT;
+                    vis = lim_t >= KT ? ~0ull : ((1ull << lim_t) - 1ull);
+                } else {
+                    mk.masked = true;
+                    vis = g_anc[node][t - ntp];
+                }
+                vis >>= half * 4;
+                mk.vis_lo = (unsigned)vis;
+                mk.vis_hi = (unsigned)(vis >> 32);
+            };
+            // End of period j: this wave's loads of K_{j+3} and V_{j+2}, all at
+            // once. (LDS-DMA writes slow down the LDS operand reads of every wave
+            // of the CU; one burst per period costs far less than loads spread
+            // between the MFMAs.) The K half they refill last held K_{j-1}, the V
+            // half V_{j-2}, both read before the barrier that opened period j.
+            // Then the page ids of K_{j+4}, by scalar loads that complete by the
+            // next barrier.
+            auto close_period = [&](int j) {
+                if (j + 2 < T) {                   // V_{j+2}: the addresses of K_{j+2}
+                    if (fast) ld.issue_fast(foff, true, (ta + j + 2) & (NS - 1), wave_u);
+                    else issue_half(j + 2, true, bk);
+                }
+                if (j + 3 < T) {
+                    fast = !SMALL && ld.fast_offset(p, ta + j + 3, wave_u, pk[0], foff);
+                    if (fast) {
+                        ld.issue_fast(foff, false, (ta + j + 3) & (NS - 1), wave_u);
                     } else {
-                        have_k = i < T;
-                        have_v = true;
-                        stage_k = (ta + i) & (NS - 1);
-                        stage_v = (ta + i - 1) & (NS - 1);
-                        if (have_k) cur = ld.blocks(p, ta + i, wave_u, pk);
+                        if (!(SMALL && ta + j + 3 < ntp)) bk = blocks_of(j + 3);
+                        issue_half(j + 3, false, bk);
                     }
                 }
+                ld.fetch_pages(p, b, ta + j + 4, wave_u, pk);
             };
-            // Loads of batch j+2 during matrix j: full batches in the steady
-            // state, the tail checks which halves exist.
-            auto hook_full = [&](int gi) {
-                if (SMALL) return;
-                #pragma unroll
-                for (int k = 0; k < 2 * LPT; ++k) {
-                    if (k * 8 / (2 * LPT) != gi) continue;
-                    if (k < LPT) ld.issue_one(cur, false, stage_k, wave_u, k);
-                    else ld.issue_one(last, true, stage_v, wave_u, k - LPT);
-                }
+            int j = 0;
+            auto run = [&](auto prev, auto cur) {
+                constexpr bool P_ = decltype(prev)::value, C_ = decltype(cur)::value;
+                const int jj = j;
+                tile_period<D, P_, C_>(st, s0, s1, C_ ? kaddr_of(ta + jj) : 0u,
+                                       P_ ? vaddr_of(ta + jj - 1) : 0u, mk, p.scale_log2);
+                if (C_) close_period(jj);
             };
-            auto hook = [&](int gi) {
-                if (SMALL) return;
-                #pragma unroll
-                for (int k = 0; k < 2 * LPT; ++k) {
-                    if (k * 8 / (2 * LPT) != gi) continue;
-                    if (k < LPT) {
-                        if (have_k) ld.issue_one(cur, false, stage_k, wave_u, k);
-                    } else if (have_v) {
-                        ld.issue_one(last, true, stage_v, wave_u, k - LPT);
-                    }
-                }
+            // Before the last PV: V of the last tile has landed for every wave.
+            auto close_periods = [&]() {
+                wait_vm_at_most(0);
+                lds_barrier();
             };
-            auto close_matrix = [&]() {
-                if (!SMALL && have_v) last = cur;
-            };
-            auto softmax = [&](int j) {
-                if (grp == 1) wait_vm_at_most(batch_loads(j + 2));
-                __builtin_amdgcn_s_setprio(0);
-                phase_barrier();
-                softmax_phase<D>(st, p, ta + j, ntp, L, node, half);
-                fetch(j + 3);          // ids for the batch issued at the next matrix phase
-            };
-            open_matrix(0);
-            matrix_phase<D, false, true>(st, kaddr_of(ta), 0u, hook);
-            close_matrix();
-            softmax(0);
-            int j = 1;
-            for (; j + 2 < T; ++j) {                 // batch j+2 is full
-                open_matrix(j);
-                matrix_phase<D, true, true>(st, kaddr_of(ta + j), vaddr_of(ta + j - 1), hook_full);
-                close_matrix();
-                softmax(j);
+            using T_ = std::true_type;
+            using F_ = std::false_type;
+            open_period(0);
+            run(F_{}, T_{});
+            for (j = 1; j < T; ++j) {
+                open_period(j);
+                run(T_{}, T_{});
             }
-            for (; j < T; ++j) {
-                open_matrix(j);
-                matrix_phase<D, true, true>(st, kaddr_of(ta + j), vaddr_of(ta + j - 1), hook);
-                close_matrix();
-                softmax(j);
-            }
-            open_matrix(T);
-            matrix_phase<D, true, false>(st, 0u, vaddr_of(ta + T - 1), hook);
-            if (grp == 0 && NW >= 2) phase_barrier();
+            close_periods();
+            run(T_{}, F_{});                   // PV of the last tile
             ta = tb;
             __syncthreads();               // ring and page ids are reused next
         }
