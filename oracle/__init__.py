@@ -20,12 +20,17 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# TREEVERIFY_ORACLE_LIB names a prebuilt oracle library to load instead (the
+# sanitizer test builds one with AddressSanitizer and UBSan).
+_LIB_OVERRIDE = os.environ.get("TREEVERIFY_ORACLE_LIB")
+_LIB = _LIB_OVERRIDE or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 
 def build(force: bool = True) -> str:
     """Compile oracle.c with gcc (fp64, no fast-math, no FMA contraction)."""
+    if _LIB_OVERRIDE:
+        return _LIB
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp%d" % os.getpid()
         cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",

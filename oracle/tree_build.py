@@ -21,9 +21,16 @@ What is computed, per sequence (the steps follow Alg. 1 in the paper's order):
 Readings where the paper is silent (each one is also a row of the design
 notes):
 
+* What a table entry is: §4.1 adds RMSNorm(E'(t)) to the logits of the step
+  after token t, §5.1 collapses E' into a lookup table and says sampling does
+  no further computation on it, so a stored row is taken to be the already
+  normalised vector RMSNorm(E'(t)) (the normalisation of a fixed row is a
+  constant, computed offline over the whole row). Entry (row, col) is that
+  vector's component for candidate col, added to the logit as it is.
 * The token-info table only covers the hot tokens (§6.1 keeps token-info for
   the 32K most frequent tokens only): `table` is [H, H] over the hot list
-  `hot`, row = the node's token, column = the candidate token. A node whose
+  `hot`, row = the node's token, column = the candidate token, i.e. the
+  normalised rows above restricted to hot rows and hot columns. A node whose
   token is not hot adds nothing; a candidate that is not hot gets nothing
   added. Table entries are bf16; the sum l + r is formed in fp32, the precision
   of the logits, and top-k decisions are taken on these fp32 sums.

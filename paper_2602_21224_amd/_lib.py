@@ -15,7 +15,9 @@ import os
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libtreeverify.so")
+# TREEVERIFY_LIB names another build of the same library to load (the
+# sanitizer test loads one whose host code carries AddressSanitizer and UBSan).
+LIB_PATH = os.environ.get("TREEVERIFY_LIB") or os.path.join(HERE, "libtreeverify.so")
 
 _lib = None
 
