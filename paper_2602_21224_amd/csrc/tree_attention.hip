@@ -44,8 +44,10 @@
 //     s_barrier, so the compiler never inserts a blanket wait for the
 //     in-flight tile loads.
 //   * Tree visibility is a per-node ancestor bit set (256 bits) in LDS, built
-//     by one wave with pointer doubling over the parent links while the first
-//     tiles load; a masked score is replaced by -inf (selected, never added).
+//     by one wave while the first tiles load: for trees of up to 64 nodes each
+//     lane follows its node's parent links through cross-lane shuffles, larger
+//     trees use pointer doubling in LDS. A masked score is replaced by -inf
+//     (selected, never added).
 #include "tv_internal.h"
 
 namespace tv {
@@ -241,13 +243,11 @@ __device__ void load_pages(const AttnParams &p, int b, int first, int npages) {
 // twice as far (cross-lane reads see the values of the previous round), until
 // no lane has an ancestor left. The caller's next workgroup barrier publishes
 // g_anc.
-__device__ void build_ancestor_masks_wave(const AttnParams &p, int b) {
+// `pi` is node `lane`'s parent as loaded by the caller (any value for lanes >= N).
+__device__ void build_ancestor_masks_wave(const AttnParams &p, int pi) {
     const int lane = threadIdx.x & (kWave - 1);
     int j = -1;
-    if (lane < p.N) {
-        const int pi = p.parent[(size_t)b * p.N + lane];
-        j = (pi < -1 || pi >= lane) ? -1 : pi;        // contract violation: treat as a root
-    }
+    if (lane < p.N) j = (pi < -1 || pi >= lane) ? -1 : pi;   // contract violation: treat as a root
     unsigned long long anc = lane < p.N ? (1ull << lane) : 0ull;
     while (__any(j >= 0)) {
         const int src = j >= 0 ? j : lane;
@@ -794,20 +794,37 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         if (t_end <= t0) continue;                    // only set-up tiles of this unit
         const bool complete = (t0 == 0 && t_end == ulen);
 
-        // ---- this wave's 32 query rows: Q fragments stay in registers
+        // Parent links for the ancestor sets (trees of up to 64 nodes), loaded
+        // before any other load of the piece so that waiting for them never
+        // waits for the tile loads behind them.
+        const bool has_tree = t_end > ntp;
+        const bool need_anc = has_tree && anc_b != b;
+        int par_pre = -1;
+        if (need_anc && wave_u == 0 && p.N <= kWave && lane < p.N)
+            par_pre = p.parent[(size_t)b * p.N + lane];
+
+        // Page ids of the first four tiles (scalar loads), ahead of the Q loads
+        // so that their latency overlaps them; later sub-ranges fetch their own.
+        int ids[4][Issue::kLoadsPerWave];
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, t0 + i, wave_u, ids[i]);
+
+        // ---- this wave's 32 query rows: Q fragments stay in registers. A row
+        // past the unit's last one loads the unit's first row instead (rows are
+        // independent through both products and the softmax, and such rows are
+        // never stored), so the loads need no branch and nothing waits for them
+        // before the first score product.
         const int row = rb * p.rows_per_block + wave_u * kRowsPerWave + col;
         const bool row_ok = row < rows_b;
-        const int node = row_ok ? row / p.G : 0;
-        const int hq = g * p.G + (row_ok ? row % p.G : 0);
+        const int qrow = row_ok ? row : rb * p.rows_per_block;
+        const int node = qrow / p.G;
+        const int hq = g * p.G + qrow % p.G;
         WaveState<D> st;
         {
             const uint16_t *qp = p.q + (((size_t)b * p.N + node) * p.Hq + hq) * D + half * 8;
             #pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
-                u16x8 v = row_ok ? *reinterpret_cast<const u16x8 *>(qp + ks * 16)
-                                 : u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-                st.qf[ks] = __builtin_bit_cast(bf16x8, v);
-            }
+            for (int ks = 0; ks < NKS; ++ks)
+                st.qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8 *>(qp + ks * 16));
         }
         #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
@@ -818,7 +835,6 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         st.l_run = 0.f;
 
         const int npages = (L + p.P - 1) >> p.p_shift;
-        const bool has_tree = t_end > ntp;
         auto kaddr_of = [&](int t) { return ring_base + (t & (NS - 1)) * Gm::kStageBytes + k_lane; };
         auto vaddr_of = [&](int t) {
             return ring_base + (t & (NS - 1)) * Gm::kStageBytes + Gm::kTileBytes + v_lane;
@@ -840,7 +856,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             // page ids in LDS only for pages shorter than a load block; ancestor
             // sets only when this piece reaches the tree tiles and the workgroup
             // has not built them for this sequence already
-            const bool want_anc = first && has_tree && anc_b != b;
+            const bool want_anc = first && need_anc;
             if (SMALL && ta < ntp) load_pages<NT>(p, b, page_first, npages);
 
             const int T = tb - ta;
@@ -862,9 +878,6 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             };
             ld.set_unit(p, b, g, L, ntp, nodes);
             {
-                int ids[4][LPT];
-                #pragma unroll
-                for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, ta + i, wave_u, ids[i]);
                 typename Issue::Blocks b0, b1;
                 #pragma unroll
                 for (int k = 0; k < LPT; ++k) pk[k] = ids[0][k];
@@ -891,7 +904,8 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             // registers up to 64 nodes, else in LDS.
             if (want_anc) {
                 if (wave_u == 0) {
-                    if (p.N <= kWave) build_ancestor_masks_wave(p, b);
+                    tie(par_pre);              // first use here, behind the tile loads
+                    if (p.N <= kWave) build_ancestor_masks_wave(p, par_pre);
                     else build_ancestor_masks_wave_lds(p, b);
                 }
                 anc_b = b;
@@ -972,52 +986,65 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             close_periods();
             run(T_{}, F_{});                   // PV of the last tile
             ta = tb;
+            if (ta < t_end) {
+                #pragma unroll
+                for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, ta + i, wave_u, ids[i]);
+            }
             __syncthreads();               // ring and page ids are reused next
         }
 
         // ---- finish the segment
+        // The normalised rows leave through this wave's slice of the (now idle)
+        // LDS ring, transposed there so that every global store writes whole
+        // rows (16 lanes x 16 bytes per 256-byte row) instead of 8-byte pieces
+        // of 32 rows. A complete unit writes out and lse; a piece of a split
+        // unit writes its output normalised by its own sum (bf16) and its (max,
+        // sum) pair (fp32): slot 0 holds the piece that continues a unit from
+        // before this share, slot 1 the one that starts inside it.
         const float l_tot = halves_sum(st.l_run);
-        if (complete) {
-            if (row_ok) {
-                const float inv = 1.f / l_tot;
-                uint16_t *op = p.out + (((size_t)b * p.N + node) * p.Hq + hq) * D;
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        constexpr int kPitch = D * 2 + 16;                   // LDS bytes per row (padded)
+        constexpr int kRowChunks = D / 8;                     // 16-byte chunks per row
+        constexpr int kRowsPerPass = kWave / kRowChunks;
+        unsigned char *wbuf = g_ring + wave_u * kRowsPerWave * kPitch;
+        #pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+            #pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                bf16x4 v;
                 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt)
-                    #pragma unroll
-                    for (int q4 = 0; q4 < 4; ++q4) {
-                        bf16x4 v;
-                        #pragma unroll
-                        for (int i = 0; i < 4; ++i) v[i] = (__bf16)(st.o[dt][q4 * 4 + i] * inv);
-                        *reinterpret_cast<bf16x4 *>(op + dt * 32 + q4 * 8 + half * 4) = v;
-                    }
-                if (p.lse && half == 0)
+                for (int i = 0; i < 4; ++i) v[i] = (__bf16)(st.o[dt][q4 * 4 + i] * inv);
+                *reinterpret_cast<bf16x4 *>(wbuf + col * kPitch + (dt * 32 + q4 * 8 + half * 4) * 2) = v;
+            }
+        const int slot = w * 2 + (unit_real_start <= start ? 0 : 1);
+        #pragma unroll
+        for (int k = 0; k < kRowsPerWave / kRowsPerPass; ++k) {
+            const int r = k * kRowsPerPass + lane / kRowChunks, ch = lane % kRowChunks;
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(wbuf + r * kPitch + ch * 16);
+            const int rl = wave_u * kRowsPerWave + r;           // row within the unit's block
+            if (complete) {
+                const int ur = rb * p.rows_per_block + rl;
+                if (ur < rows_b) {
+                    const int nd = ur / p.G, h = g * p.G + ur % p.G;
+                    *reinterpret_cast<u32x4 *>(p.out + (((size_t)b * p.N + nd) * p.Hq + h) * D + ch * 8) = v;
+                }
+            } else {
+                *reinterpret_cast<u32x4 *>(p.ws_o + ((size_t)slot * p.rows_per_block + rl) * D + ch * 8) = v;
+            }
+        }
+        if (half == 0) {
+            if (complete) {
+                if (row_ok && p.lse)
                     p.lse[((size_t)b * p.N + node) * p.Hq + hq] =
                         st.m_run * p.scale + __builtin_amdgcn_logf(l_tot) * kLn2;
-            }
-        } else {
-            // A piece of a split unit: its output normalised by its own sum, in
-            // bf16, plus the (max, sum) pair in fp32. Slot 0 holds the piece that
-            // continues a unit from before this share, slot 1 the one that starts
-            // inside it.
-            const int slot = w * 2 + (unit_real_start <= start ? 0 : 1);
-            const int rloc = wave_u * kRowsPerWave + col;
-            uint16_t *po = p.ws_o + ((size_t)slot * p.rows_per_block + rloc) * D;
-            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-            #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-                #pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    bf16x4 v;
-                    #pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] = (__bf16)(st.o[dt][q4 * 4 + i] * inv);
-                    *reinterpret_cast<bf16x4 *>(po + dt * 32 + q4 * 8 + half * 4) = v;
-                }
-            if (half == 0) {
+            } else {
+                const int rloc = wave_u * kRowsPerWave + col;
                 float *pm = p.ws_ml + ((size_t)slot * p.rows_per_block + rloc) * 2;
                 pm[0] = (st.m_run == kNegInf) ? kNegInf : st.m_run * p.scale_log2;
                 pm[1] = l_tot;
             }
         }
+        __syncthreads();                   // the ring is refilled by the next piece
     }
 
     // Rows of padding nodes (at or past a sequence's node count) are not part
