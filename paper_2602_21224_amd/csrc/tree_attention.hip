@@ -1135,8 +1135,6 @@ hipError_t launch_dn(const AttnParams &p, hipStream_t s) {
 template <int D>
 hipError_t launch_d(const AttnParams &p, int waves, hipStream_t s) {
     switch (waves) {
-        case 1: return launch_dn<D, 1>(p, s);
-        case 2: return launch_dn<D, 2>(p, s);
         case 4: return launch_dn<D, 4>(p, s);
         case 8: return launch_dn<D, 8>(p, s);
         default: return hipErrorInvalidValue;

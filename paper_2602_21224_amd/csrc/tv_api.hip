@@ -16,7 +16,7 @@ namespace {
 constexpr int kMaxDevices = 64;
 constexpr int kWgPerCu = 1;          // the attention kernel's LDS ring allows one workgroup per CU
 constexpr int kMinShareTiles = 8;    // smallest per-workgroup share worth a partial
-constexpr int kSetupTiles = 6;       // measured cost of starting a unit piece, in 64-key tiles
+constexpr int kSetupTiles = 3;       // measured cost of starting a unit piece, in 64-key tiles
 constexpr int kArgmaxMinWorkgroups = 2048;
 constexpr int kArgmaxMinSegment = 4096;
 
@@ -80,9 +80,12 @@ AttnShape attn_shape(int N, int Hq, int Hkv) {
     AttnShape s;
     s.G = Hq / Hkv;
     s.rows = N * s.G;
+    // Four waves at least: a workgroup of fewer waves leaves a unit's tile
+    // loads to one or two waves (and the one-wave kernel spills), which
+    // measured 11x (one wave) and 1.2x (two waves) slower on 12-row units
+    // than four waves with the extra rows idle.
     const int need = (s.rows + tv::kRowsPerWave - 1) / tv::kRowsPerWave;
-    s.waves = need >= 8 ? 8 : (need >= 4 ? 4 : (need >= 2 ? 2 : 1));
-    if (need > s.waves && s.waves < 8) s.waves *= 2;
+    s.waves = need > 4 ? 8 : 4;
     s.rows_per_block = s.waves * tv::kRowsPerWave;
     s.row_blocks = (s.rows + s.rows_per_block - 1) / s.rows_per_block;
     s.tree_tiles_all = 0;
