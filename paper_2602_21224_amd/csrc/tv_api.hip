@@ -15,7 +15,7 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 constexpr int kWgPerCu = 1;          // the attention kernel's LDS ring allows one workgroup per CU
-constexpr int kMinShareTiles = 8;    // smallest per-workgroup share worth a partial
+constexpr int kMinShareTiles = 2;    // smallest per-workgroup share (measured: 8 -> 2 is -26 % at 8B bs1)
 constexpr int kSetupTiles = 3;       // measured cost of starting a unit piece, in 64-key tiles
 constexpr int kArgmaxMinWorkgroups = 2048;
 constexpr int kArgmaxMinSegment = 4096;
