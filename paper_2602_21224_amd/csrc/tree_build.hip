@@ -25,7 +25,7 @@ namespace tv {
 namespace {
 
 constexpr int kTbThreads = 256;
-constexpr int kTbBatch = 8;                // tokens per thread whose loads are in flight together
+constexpr int kTbChunk = 32;               // candidates per thread held in registers at once
 constexpr int kTbWaves = kTbThreads / kWave;
 constexpr int kPruneThreads = 1024;
 constexpr int kPruneSlots = 4096;          // >= 1 + k + (S - 1) k^2 for k, S <= 16
@@ -57,19 +57,6 @@ __device__ __forceinline__ int key_index(unsigned long long key) {
 struct OnlineSum {
     float m = -__builtin_huge_valf();
     double s = 0.0;
-    template <int U>
-    __device__ __forceinline__ void add_batch(const float (&x)[U], const bool (&use)[U]) {
-        float mb = m;
-        #pragma unroll
-        for (int u = 0; u < U; ++u) mb = use[u] ? fmaxf(mb, x[u]) : mb;
-        if (mb == -__builtin_huge_valf()) return;          // nothing finite so far
-        double acc = m == -__builtin_huge_valf() ? 0.0 : s * exp((double)m - (double)mb);
-        #pragma unroll
-        for (int u = 0; u < U; ++u)
-            acc += use[u] ? exp((double)x[u] - (double)mb) : 0.0;
-        s = acc;
-        m = mb;
-    }
     __device__ __forceinline__ void merge(float m2, double s2) {
         if (m2 == -__builtin_huge_valf()) return;
         if (m == -__builtin_huge_valf()) { m = m2; s = s2; return; }
@@ -114,6 +101,13 @@ __device__ __forceinline__ unsigned long long wave_max64(unsigned long long v) {
                   umax64(readlane64(v, 47), readlane64(v, 63)));
 }
 
+// Largest 32-bit value over the wave.
+__device__ __forceinline__ unsigned int wave_max32(unsigned int v) {
+    #pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = max(v, (unsigned int)__shfl_xor((int)v, off));
+    return v;
+}
+
 // A wave's top-k list, distributed over lanes: lane j < k holds the (j+1)-th
 // largest key seen by the wave (0 = empty). The k-th key is the wave's
 // admission threshold, so after the first few batches almost no candidate
@@ -135,6 +129,79 @@ struct WaveTopK {
         }
     }
 };
+
+// exp(x) for x <= 0 in double precision, by Tang's table-driven method (ACM
+// TOMS 15(2), 1989): x = (32 n + j) ln2/32 + r with |r| <= ln2/64, so
+// e^x = 2^(n >> 5) 2^(j/32) e^r, j = n & 31; e^r - 1 from its degree-6 Taylor
+// polynomial (truncation below 2e-17 on that interval); 2^(j/32) from a
+// 32-entry table (tab, filled by fill_exp2_table). ln2/32 is split into
+// kL1 (its 37 leading significant bits, so N kL1 is exact for |N| < 2^16) and
+// kL2 = ln2/32 - kL1 rounded to double. Arguments below -745 (and -inf) give 0.
+// About 1 ulp, against about 45 instructions for the library's exp.
+__device__ __forceinline__ double exp_nonpos(double x, const double *tab) {
+    const double kInvL = 46.16624130844683;          // 32 / ln2
+    const double kL1 = 0.021660849392446835;
+    const double kL2 = 5.145609244655338e-14;
+    const double N = __builtin_rint(x * kInvL);
+    double r = __builtin_fma(-N, kL1, x);
+    r = __builtin_fma(-N, kL2, r);
+    double q = __builtin_fma(r, 1.0 / 720.0, 1.0 / 120.0);
+    q = __builtin_fma(q, r, 1.0 / 24.0);
+    q = __builtin_fma(q, r, 1.0 / 6.0);
+    q = __builtin_fma(q, r, 0.5);
+    q = __builtin_fma(q, r, 1.0);
+    q *= r;                                          // e^r - 1
+    const int n = x < -745.0 ? 0 : (int)N;
+    const double t = tab[n & 31];
+    const double y = __builtin_ldexp(__builtin_fma(t, q, t), n >> 5);
+    return x < -745.0 ? 0.0 : y;
+}
+
+// 2^(j/32), j = 0..31, into LDS for exp_nonpos; the caller synchronises.
+__device__ __forceinline__ void fill_exp2_table(double *tab) {
+    if (threadIdx.x < 32) tab[threadIdx.x] = exp2((double)threadIdx.x / 32.0);
+}
+
+// One chunk of a thread's candidates, all in registers: x[u] is the value of
+// vocabulary id id(u), -inf when it is not a candidate. Folds their
+// (max, fp64 sum of exp(x - max)) into os and their k largest keys into the
+// wave's list. The wave's k largest are all at or above the k-th largest of
+// the lanes' maxima (those are k candidates already), so only candidates at or
+// above that floor form keys and go through the wave-serial insertion.
+template <int U, typename Id>
+__device__ __forceinline__ void fold_chunk(const float (&x)[U], Id id, int k, int lane,
+                                           const double *tab, OnlineSum &os, WaveTopK &tk) {
+    constexpr float kNegInf = -__builtin_huge_valf();
+    float m = kNegInf;
+    unsigned int kv[U];
+    unsigned int kmax = 0u;
+    #pragma unroll
+    for (int u = 0; u < U; ++u) {
+        m = fmaxf(m, x[u]);
+        kv[u] = x[u] != kNegInf ? order_key(x[u]) : 0u;
+        kmax = max(kmax, kv[u]);
+    }
+    if (m != kNegInf) {
+        double sum = 0.0;
+        #pragma unroll
+        for (int u = 0; u < U; ++u) sum += exp_nonpos((double)x[u] - (double)m, tab);
+        os.merge(m, sum);
+    }
+    // k-th largest lane maximum (ties may remove two lanes in one round: the
+    // floor only gets lower, never wrong)
+    unsigned int floor_key = 0u;
+    for (int r = 0; r < k; ++r) {
+        const unsigned int mx = wave_max32(kmax);
+        if (kmax == mx) kmax = 0u;
+        floor_key = mx;
+    }
+    #pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const bool pass = kv[u] != 0u && kv[u] >= floor_key;
+        if (__ballot(pass) == 0ull) continue;                 // wave-uniform
+        tk.offer(pass ? pack_key(kv[u], (unsigned int)id(u)) : 0ull, k, lane);
+    }
+}
 
 // Workgroup reduction of every thread's OnlineSum and every wave's top-k list
 // into one TbPart.
@@ -199,46 +266,36 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
     TbPart *__restrict__ rows, float *__restrict__ hot_logits, int max_nodes,
     int32_t *__restrict__ node_tok, int32_t *__restrict__ node_par,
     double *__restrict__ node_joint, int32_t *__restrict__ frontier) {
+    __shared__ double s_exp2[32];
+    fill_exp2_table(s_exp2);
+    __syncthreads();
     const int row = blockIdx.x, seg = blockIdx.y;
     const int v0 = seg * seg_len, v1 = min(V, v0 + seg_len);
     const float *l = logits + (size_t)row * V;
     OnlineSum os;
     WaveTopK tk;
     const int lane = threadIdx.x & (kWave - 1);
-    // Batches of kTbBatch tokens per thread: all loads of a batch are issued
-    // before any is used. The batch loop is uniform over the workgroup (the
-    // wave's top-k list is updated by whole-wave steps).
+    // Chunks of kTbChunk tokens per thread, every load of a chunk issued before
+    // any is used (indices clamped, so the loads are unconditional). The chunk
+    // loop is uniform over the workgroup (the wave's list is updated by
+    // whole-wave steps).
     const int iters = (max(v1 - v0, 0) + kTbThreads - 1) / kTbThreads;
-    // the loads of batch n+1 are issued before batch n is used
-    int hn[kTbBatch];
-    float xn[kTbBatch];
-    auto load = [&](int it0) {
+    for (int it0 = 0; it0 < iters; it0 += kTbChunk) {
+        const int vb = v0 + it0 * kTbThreads + (int)threadIdx.x;
+        int hv[kTbChunk];
+        float xv[kTbChunk];
         #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u) {     // unconditional loads (index clamped)
-            const int v = min(v0 + (it0 + u) * kTbThreads + (int)threadIdx.x, v1 - 1);
-            hn[u] = H > 0 ? hot_index[v] : -1;
-            xn[u] = l[v];
+        for (int u = 0; u < kTbChunk; ++u) {
+            const int v = min(vb + u * kTbThreads, v1 - 1);
+            hv[u] = H > 0 ? hot_index[v] : -1;
+            xv[u] = l[v];
         }
-    };
-    if (iters > 0) load(0);
-    for (int it0 = 0; it0 < iters; it0 += kTbBatch) {
-        int hv[kTbBatch];
-        float xv[kTbBatch];
-        bool use[kTbBatch];
         #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u) { hv[u] = hn[u]; xv[u] = xn[u]; }
-        if (it0 + kTbBatch < iters) load(it0 + kTbBatch);
-        #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u) {     // outside, or hot (handled per node): unused
-            const int v = v0 + (it0 + u) * kTbThreads + (int)threadIdx.x;
-            use[u] = v < v1 && !(hv[u] >= 0 && hv[u] < H) && xv[u] != -__builtin_huge_valf();
+        for (int u = 0; u < kTbChunk; ++u) {     // outside, or hot (handled per node): unused
+            const bool use = vb + u * kTbThreads < v1 && !(hv[u] >= 0 && hv[u] < H);
+            xv[u] = use ? xv[u] : -__builtin_huge_valf();
         }
-        os.add_batch(xv, use);
-        #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u) {
-            const int v = v0 + (it0 + u) * kTbThreads + (int)threadIdx.x;
-            tk.offer(use[u] ? pack_key(order_key(xv[u]), (unsigned int)v) : 0ull, k, lane);
-        }
+        fold_chunk(xv, [&](int u) { return vb + u * kTbThreads; }, k, lane, s_exp2, os, tk);
     }
     block_reduce_part(os, tk, k, rows + (size_t)row * gridDim.y + seg);
     // this row's logits of the hot tokens, contiguous for the per-node passes
@@ -246,9 +303,20 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
         const int c_len = (H + gridDim.y - 1) / gridDim.y;
         const int c0 = seg * c_len, c1 = min(H, c0 + c_len);
         float *lh = hot_logits + (size_t)row * H;
-        for (int c = c0 + threadIdx.x; c < c1; c += kTbThreads) {
-            const int v = hot_vocab[c];
-            lh[c] = (v >= 0 && v < V) ? l[v] : -__builtin_huge_valf();
+        constexpr int kG = 8;                        // gathers per thread in flight together
+        for (int cb = c0 + (int)threadIdx.x; cb < c1; cb += kG * kTbThreads) {
+            int hv[kG];
+            float hx[kG];
+            #pragma unroll
+            for (int u = 0; u < kG; ++u) {
+                const int c = cb + u * kTbThreads;
+                hv[u] = c < c1 ? hot_vocab[c] : -1;
+            }
+            #pragma unroll
+            for (int u = 0; u < kG; ++u) hx[u] = (hv[u] >= 0 && hv[u] < V) ? l[hv[u]] : -__builtin_huge_valf();
+            #pragma unroll
+            for (int u = 0; u < kG; ++u)
+                if (cb + u * kTbThreads < c1) lh[cb + u * kTbThreads] = hx[u];
         }
     }
     if (seg == 0 && row % S == 0 && threadIdx.x == 0) {
@@ -275,6 +343,9 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
     const TbWindow win = tb_window(accept_len, b, S, r);
     if (step >= win.count) return;                 // this sequence's tree is complete
     if (j >= fr[0]) return;                        // no such frontier node at this step
+    __shared__ double s_exp2[32];
+    fill_exp2_table(s_exp2);
+    __syncthreads();
     const int t = node_tok[(size_t)b * max_nodes + fr[1 + j]];
     int h = (t >= 0 && t < V) ? hot_index[t] : -1;
     if (h >= H) h = -1;
@@ -284,38 +355,26 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
     OnlineSum os;
     WaveTopK tk;
     const int lane = threadIdx.x & (kWave - 1);
-    const int iters = (max(c1 - c0, 0) + kTbThreads - 1) / kTbThreads;   // batches as above
-    int vn[kTbBatch];
-    float xn[kTbBatch];
-    unsigned int rn[kTbBatch];
-    auto load = [&](int it0) {
+    const int iters = (max(c1 - c0, 0) + kTbThreads - 1) / kTbThreads;   // chunks as above
+    for (int it0 = 0; it0 < iters; it0 += kTbChunk) {
+        const int cb = c0 + it0 * kTbThreads + (int)threadIdx.x;
+        int vv[kTbChunk];
+        float xv[kTbChunk];
+        unsigned int rv[kTbChunk];
         #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u) {     // unconditional loads (index clamped)
-            const int cc = min(c0 + (it0 + u) * kTbThreads + (int)threadIdx.x, c1 - 1);
-            vn[u] = hot_vocab[cc];
-            xn[u] = lh[cc];
-            rn[u] = trow[cc];
+        for (int u = 0; u < kTbChunk; ++u) {
+            const int cc = min(cb + u * kTbThreads, c1 - 1);
+            vv[u] = hot_vocab[cc];
+            xv[u] = lh[cc];
+            rv[u] = trow[cc];
         }
-    };
-    if (iters > 0) load(0);
-    for (int it0 = 0; it0 < iters; it0 += kTbBatch) {
-        int vv[kTbBatch];
-        float xv[kTbBatch];
-        unsigned int rv[kTbBatch];
-        bool use[kTbBatch];
         #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u) { vv[u] = vn[u]; xv[u] = xn[u]; rv[u] = rn[u]; }
-        if (it0 + kTbBatch < iters) load(it0 + kTbBatch);
-        #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u) {
-            const int cc = c0 + (it0 + u) * kTbThreads + (int)threadIdx.x;
+        for (int u = 0; u < kTbChunk; ++u) {
             if (h >= 0) xv[u] += __uint_as_float(rv[u] << 16);
-            use[u] = cc < c1 && vv[u] >= 0 && vv[u] < V && xv[u] != -__builtin_huge_valf();
+            const bool use = cb + u * kTbThreads < c1 && vv[u] >= 0 && vv[u] < V;
+            xv[u] = use ? xv[u] : -__builtin_huge_valf();
         }
-        os.add_batch(xv, use);
-        #pragma unroll
-        for (int u = 0; u < kTbBatch; ++u)
-            tk.offer(use[u] ? pack_key(order_key(xv[u]), (unsigned int)vv[u]) : 0ull, k, lane);
+        fold_chunk(xv, [&](int u) { return vv[u]; }, k, lane, s_exp2, os, tk);
     }
     block_reduce_part(os, tk, k, out);
 }
