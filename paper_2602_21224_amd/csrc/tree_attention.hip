@@ -710,7 +710,122 @@ __device__ __forceinline__ void tile_period(WaveState<D> &st, f32x16 &sc0, f32x1
     }
 }
 
-template <int D, int NW, bool SMALL>
+// ---- units of at most 16 query rows (the paper's own MHA shape: 12 nodes x 1
+// head per KV head). Every row tile of the main scheme would be mostly empty,
+// so here the workgroup's waves take the unit's tiles in turn (tile j belongs
+// to wave j mod NW) and compute it whole with v_mfma_f32_16x16x32_bf16: keys on
+// M (16 per block, 4 blocks per tile), the 16 rows on N, head dim on K. Lane l
+// holds row l % 16; in a 16x16 accumulator it holds entries m = 4 (l / 16) + i,
+// i < 4, so S gives it keys 16 kb + 4 (l / 16) + i of every key block kb. The
+// PV product takes P^T straight from there: its k-step over key blocks (kb0,
+// kb1) pairs k = 8 (l / 16) + i with key 16 kb0 + 4 (l / 16) + i and
+// k = 8 (l / 16) + 4 + i with key 16 kb1 + 4 (l / 16) + i, and the V^T operand
+// is read with the same key order through ds_read_b64_tr_b16 (a 16-lane group
+// reads 4 key rows x 16 head-dim columns; lane i of the group receives column
+// i of the 4 rows). Each wave keeps its own running max, sum and O^T for its
+// tiles; the waves' states are combined with the log-sum-exp rule at the end
+// of the piece. Tile loads stay cooperative (all waves, one barrier per tile),
+// and with one wave computing per tile the period is bound by the loads.
+template <int D>
+struct NarrowState {
+    static constexpr int NKS = D / 32;     // k-steps over the head dim (S)
+    static constexpr int NDB = D / 16;     // 16-wide head-dim blocks of O^T
+    bf16x8 qf[NKS];
+    f32x4 o[NDB];
+    float m_run, msc, l_run;
+};
+
+// Tile j for the owning wave. kaddr/vaddr: the stage's K and V tile bases (LDS
+// byte addresses); vis: the visible keys of the lane's row (bit = key in tile),
+// all ones for a full prefix tile.
+template <int D>
+__device__ __forceinline__ void narrow_tile(NarrowState<D> &st, unsigned kbase, unsigned vbase,
+                                            bool masked, unsigned long long vis, float c, int lane) {
+    using Gm = Geo<D>;
+    constexpr int C = Gm::kChunks;
+    constexpr int NKS = D / 32, NDB = D / 16;
+    const int g = lane >> 4, i16 = lane & 15;
+    // S^T blocks
+    f32x4 sb[4];
+    #pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+        const int key = kb * 16 + i16;
+        const unsigned row = kbase + key * Gm::kRowBytes;
+        u32x4 a[NKS];
+        #pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+            asm volatile("ds_read_b128 %0, %1" : "=v"(a[ks])
+                         : "v"(row + ((unsigned)((4 * ks + g) ^ swz<C>(key % C)) << 4)));
+        lds_wait<0>();
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        #pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            tie(a[ks]);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[ks]), st.qf[ks],
+                                                          acc, 0, 0, 0);
+        }
+        sb[kb] = acc;
+    }
+    if (masked) {
+        #pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            #pragma unroll
+            for (int i = 0; i < 4; ++i)
+                sb[kb][i] = ((vis >> (kb * 16 + 4 * g + i)) & 1ull) ? sb[kb][i] : kNegInf;
+    }
+    float mt = kNegInf;
+    #pragma unroll
+    for (int kb = 0; kb < 4; ++kb) mt = fmaxf(mt, fmaxf(fmaxf(sb[kb][0], sb[kb][1]), fmaxf(sb[kb][2], sb[kb][3])));
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const bool raise = mt * c > st.m_run * c + kRescaleSlack;
+    if (__any(raise)) {
+        const float m_new = raise ? mt : st.m_run;
+        const float alpha = (st.m_run == kNegInf) ? 0.f : __builtin_amdgcn_exp2f((st.m_run - m_new) * c);
+        st.l_run *= alpha;
+        #pragma unroll
+        for (int db = 0; db < NDB; ++db)
+            #pragma unroll
+            for (int i = 0; i < 4; ++i) st.o[db][i] *= alpha;
+        st.m_run = m_new;
+    }
+    st.msc = (st.m_run == kNegInf) ? 0.f : st.m_run * c;
+    bf16x8 pb[2];
+    float ps = 0.f;
+    #pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+        #pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sb[kb][i], c, -st.msc));
+            ps += x;
+            pb[kb >> 1][(kb & 1) * 4 + i] = (__bf16)x;
+        }
+    st.l_run += ps;
+    // O^T += V^T P^T, two k-steps of 32 keys
+    #pragma unroll
+    for (int kst = 0; kst < 2; ++kst) {
+        #pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            u32x2 v[2];
+            #pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int key = (2 * kst + r) * 16 + 4 * g + (i16 >> 2);
+                const int chunk = 2 * db + ((i16 & 3) >> 1);
+                const unsigned addr = vbase + key * Gm::kRowBytes +
+                                      ((unsigned)(chunk ^ swz<C>(key % C)) << 4) + (i16 & 1) * 8;
+                asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v[r]) : "v"(addr));
+            }
+            lds_wait<0>();
+            tie(v[0]);
+            tie(v[1]);
+            const u32x4 a = {v[0][0], v[0][1], v[1][0], v[1][1]};
+            st.o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), pb[kst],
+                                                               st.o[db], 0, 0, 0);
+        }
+    }
+}
+
+template <int D, int NW, bool SMALL, bool NARROW>
 __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p) {
     using Gm = Geo<D>;
     using Issue = TileIssue<D, NW, SMALL>;
@@ -820,19 +935,35 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         const int node = qrow / p.G;
         const int hq = g * p.G + qrow % p.G;
         WaveState<D> st;
-        {
+        NarrowState<D> ns;
+        // narrow units: lane l holds row l % 16 (rows past the unit's last load
+        // its first row, never stored) and head-dim columns 8 (l / 16) + 32 ks
+        const int nrow = NARROW ? min(lane & 15, rows_b - 1) : 0;
+        const int nnode = nrow / p.G;
+        if constexpr (!NARROW) {
             const uint16_t *qp = p.q + (((size_t)b * p.N + node) * p.Hq + hq) * D + half * 8;
             #pragma unroll
             for (int ks = 0; ks < NKS; ++ks)
                 st.qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8 *>(qp + ks * 16));
-        }
-        #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
             #pragma unroll
-            for (int r = 0; r < 16; ++r) st.o[dt][r] = 0.f;
-        st.m_run = kNegInf;
-        st.msc = 0.f;
-        st.l_run = 0.f;
+            for (int dt = 0; dt < NDT; ++dt)
+                #pragma unroll
+                for (int r = 0; r < 16; ++r) st.o[dt][r] = 0.f;
+            st.m_run = kNegInf;
+            st.msc = 0.f;
+            st.l_run = 0.f;
+        } else {
+            const int nhq = g * p.G + nrow % p.G;
+            const uint16_t *qp = p.q + (((size_t)b * p.N + nnode) * p.Hq + nhq) * D + (lane >> 4) * 8;
+            #pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+                ns.qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8 *>(qp + ks * 32));
+            #pragma unroll
+            for (int db = 0; db < D / 16; ++db) ns.o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+            ns.m_run = kNegInf;
+            ns.msc = 0.f;
+            ns.l_run = 0.f;
+        }
 
         const int npages = (L + p.P - 1) >> p.p_shift;
         auto kaddr_of = [&](int t) { return ring_base + (t & (NS - 1)) * Gm::kStageBytes + k_lane; };
@@ -887,8 +1018,8 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                 b1 = blocks_of(1);
                 #pragma unroll
                 for (int k = 0; k < LPT; ++k) pk[k] = ids[2][k];
-                bk = blocks_of(2);             // K_2 now, V_2 in period 0
-                // issue order K_0, V_0, K_1, V_1, K_2 (the waits below count on it)
+                bk = blocks_of(2);             // K_2 now, V_2 in period 0 (narrow: now)
+                // issue order K_0, V_0, K_1, V_1, K_2 (, V_2) (the waits below count on it)
                 issue_half(0, false, b0);
                 issue_half(0, true, b0);
                 if (T > 1) {
@@ -896,6 +1027,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                     issue_half(1, true, b1);
                 }
                 if (T > 2) issue_half(2, false, bk);
+                if (NARROW && T > 2) issue_half(2, true, bk);
                 #pragma unroll
                 for (int k = 0; k < LPT; ++k) pk[k] = ids[3][k];
             }
@@ -917,9 +1049,11 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             // wave's later loads may still be in flight) and every wave is done
             // with period j - 1; then tile j's mask.
             TileMask mk;
+            unsigned long long nvis = ~0ull;   // narrow units: the visible keys of the lane's row
             auto open_period = [&](int j) {
                 int newer;                     // loads issued after the last one period j needs
-                if (j == 0) newer = LPT * ((T > 1 ? 2 : 0) + (T > 2 ? 1 : 0)) + LPT;   // V_0, K_1, V_1, K_2
+                if (NARROW) newer = 2 * LPT * ((j + 1 < T ? 1 : 0) + (j + 2 < T ? 1 : 0));   // tiles j+1, j+2
+                else if (j == 0) newer = LPT * ((T > 1 ? 2 : 0) + (T > 2 ? 1 : 0)) + LPT;   // V_0, K_1, V_1, K_2
                 else if (j == 1) newer = LPT * ((T > 1 ? 1 : 0) + (T > 2 ? 1 : 0)) + loads_in(0);
                 else if (j == 2) newer = loads_in(0) + loads_in(1);
                 else newer = loads_in(j - 2) + loads_in(j - 1);
@@ -933,8 +1067,9 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                     vis = lim_t >= KT ? ~0ull : ((1ull << lim_t) - 1ull);
                 } else {
                     mk.masked = true;
-                    vis = g_anc[node][t - ntp];
+                    vis = g_anc[NARROW ? nnode : node][t - ntp];
                 }
+                nvis = vis;
                 vis >>= half * 4;
                 mk.vis_lo = (unsigned)vis;
                 mk.vis_hi = (unsigned)(vis >> 32);
@@ -977,14 +1112,41 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             };
             using T_ = std::true_type;
             using F_ = std::false_type;
-            open_period(0);
-            run(F_{}, T_{});
-            for (j = 1; j < T; ++j) {
-                open_period(j);
-                run(T_{}, T_{});
+            if constexpr (NARROW) {
+                // tile t is computed whole by wave t % NW (= its ring stage); at
+                // the end of period j every wave issues its share of tile j + 3
+                // (K and V), whose stage last held tile j - 1, computed in period
+                // j - 1, before the barrier that opened period j
+                for (j = 0; j < T; ++j) {
+                    open_period(j);
+                    const int t = ta + j;
+                    if ((t & (NS - 1)) == wave_u)
+                        narrow_tile<D>(ns, ring_base + (t & (NS - 1)) * Gm::kStageBytes,
+                                       ring_base + (t & (NS - 1)) * Gm::kStageBytes + Gm::kTileBytes,
+                                       mk.masked, nvis, p.scale_log2, lane);
+                    if (j + 3 < T) {
+                        fast = !SMALL && ld.fast_offset(p, t + 3, wave_u, pk[0], foff);
+                        if (fast) {
+                            ld.issue_fast(foff, false, (t + 3) & (NS - 1), wave_u);
+                            ld.issue_fast(foff, true, (t + 3) & (NS - 1), wave_u);
+                        } else {
+                            if (!(SMALL && t + 3 < ntp)) bk = blocks_of(j + 3);
+                            issue_half(j + 3, false, bk);
+                            issue_half(j + 3, true, bk);
+                        }
+                    }
+                    ld.fetch_pages(p, b, t + 4, wave_u, pk);
+                }
+            } else {
+                open_period(0);
+                run(F_{}, T_{});
+                for (j = 1; j < T; ++j) {
+                    open_period(j);
+                    run(T_{}, T_{});
+                }
+                close_periods();
+                run(T_{}, F_{});               // PV of the last tile
             }
-            close_periods();
-            run(T_{}, F_{});                   // PV of the last tile
             ta = tb;
             if (ta < t_end) {
                 #pragma unroll
@@ -1001,47 +1163,109 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         // unit writes its output normalised by its own sum (bf16) and its (max,
         // sum) pair (fp32): slot 0 holds the piece that continues a unit from
         // before this share, slot 1 the one that starts inside it.
-        const float l_tot = halves_sum(st.l_run);
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        constexpr int kPitch = D * 2 + 16;                   // LDS bytes per row (padded)
-        constexpr int kRowChunks = D / 8;                     // 16-byte chunks per row
-        constexpr int kRowsPerPass = kWave / kRowChunks;
-        unsigned char *wbuf = g_ring + wave_u * kRowsPerWave * kPitch;
-        #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-            #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                bf16x4 v;
-                #pragma unroll
-                for (int i = 0; i < 4; ++i) v[i] = (__bf16)(st.o[dt][q4 * 4 + i] * inv);
-                *reinterpret_cast<bf16x4 *>(wbuf + col * kPitch + (dt * 32 + q4 * 8 + half * 4) * 2) = v;
-            }
         const int slot = w * 2 + (unit_real_start <= start ? 0 : 1);
-        #pragma unroll
-        for (int k = 0; k < kRowsPerWave / kRowsPerPass; ++k) {
-            const int r = k * kRowsPerPass + lane / kRowChunks, ch = lane % kRowChunks;
-            const u32x4 v = *reinterpret_cast<const u32x4 *>(wbuf + r * kPitch + ch * 16);
-            const int rl = wave_u * kRowsPerWave + r;           // row within the unit's block
-            if (complete) {
-                const int ur = rb * p.rows_per_block + rl;
-                if (ur < rows_b) {
-                    const int nd = ur / p.G, h = g * p.G + ur % p.G;
-                    *reinterpret_cast<u32x4 *>(p.out + (((size_t)b * p.N + nd) * p.Hq + h) * D + ch * 8) = v;
+        if constexpr (!NARROW) {
+            const float l_tot = halves_sum(st.l_run);
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            constexpr int kPitch = D * 2 + 16;                   // LDS bytes per row (padded)
+            constexpr int kRowChunks = D / 8;                     // 16-byte chunks per row
+            constexpr int kRowsPerPass = kWave / kRowChunks;
+            unsigned char *wbuf = g_ring + wave_u * kRowsPerWave * kPitch;
+            #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+                #pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    bf16x4 v;
+                    #pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = (__bf16)(st.o[dt][q4 * 4 + i] * inv);
+                    *reinterpret_cast<bf16x4 *>(wbuf + col * kPitch + (dt * 32 + q4 * 8 + half * 4) * 2) = v;
                 }
-            } else {
-                *reinterpret_cast<u32x4 *>(p.ws_o + ((size_t)slot * p.rows_per_block + rl) * D + ch * 8) = v;
+            #pragma unroll
+            for (int k = 0; k < kRowsPerWave / kRowsPerPass; ++k) {
+                const int r = k * kRowsPerPass + lane / kRowChunks, ch = lane % kRowChunks;
+                const u32x4 v = *reinterpret_cast<const u32x4 *>(wbuf + r * kPitch + ch * 16);
+                const int rl = wave_u * kRowsPerWave + r;           // row within the unit's block
+                if (complete) {
+                    const int ur = rb * p.rows_per_block + rl;
+                    if (ur < rows_b) {
+                        const int nd = ur / p.G, h = g * p.G + ur % p.G;
+                        *reinterpret_cast<u32x4 *>(p.out + (((size_t)b * p.N + nd) * p.Hq + h) * D + ch * 8) = v;
+                    }
+                } else {
+                    *reinterpret_cast<u32x4 *>(p.ws_o + ((size_t)slot * p.rows_per_block + rl) * D + ch * 8) = v;
+                }
             }
-        }
-        if (half == 0) {
-            if (complete) {
-                if (row_ok && p.lse)
-                    p.lse[((size_t)b * p.N + node) * p.Hq + hq] =
-                        st.m_run * p.scale + __builtin_amdgcn_logf(l_tot) * kLn2;
-            } else {
-                const int rloc = wave_u * kRowsPerWave + col;
-                float *pm = p.ws_ml + ((size_t)slot * p.rows_per_block + rloc) * 2;
-                pm[0] = (st.m_run == kNegInf) ? kNegInf : st.m_run * p.scale_log2;
-                pm[1] = l_tot;
+            if (half == 0) {
+                if (complete) {
+                    if (row_ok && p.lse)
+                        p.lse[((size_t)b * p.N + node) * p.Hq + hq] =
+                            st.m_run * p.scale + __builtin_amdgcn_logf(l_tot) * kLn2;
+                } else {
+                    const int rloc = wave_u * kRowsPerWave + col;
+                    float *pm = p.ws_ml + ((size_t)slot * p.rows_per_block + rloc) * 2;
+                    pm[0] = (st.m_run == kNegInf) ? kNegInf : st.m_run * p.scale_log2;
+                    pm[1] = l_tot;
+                }
+            }
+        } else {
+            // Narrow units: the waves' (max, sum, O^T) of the 16 rows meet in
+            // the idle ring and combine with the log-sum-exp rule; thread
+            // (row, 8-column chunk) writes one 16-byte piece of the row.
+            constexpr int kCh = D / 8;
+            float *ow = reinterpret_cast<float *>(g_ring);                 // [NW][16][D]
+            float *mlw = ow + NW * 16 * D;                                  // [NW][16][2]
+            float lw = ns.l_run;
+            lw += __shfl_xor(lw, 16);
+            lw += __shfl_xor(lw, 32);
+            #pragma unroll
+            for (int db = 0; db < D / 16; ++db)
+                *reinterpret_cast<f32x4 *>(ow + ((size_t)wave_u * 16 + (lane & 15)) * D + db * 16 +
+                                           4 * (lane >> 4)) = ns.o[db];
+            if (lane < 16) {
+                mlw[(wave_u * 16 + lane) * 2] = ns.m_run;
+                mlw[(wave_u * 16 + lane) * 2 + 1] = lw;
+            }
+            __syncthreads();
+            const int nrows = min(16, rows_b);
+            const float c = p.scale_log2;
+            for (int task = tid; task < 16 * kCh; task += NT) {
+                const int r = task / kCh, ch = task % kCh;
+                if (r >= nrows) continue;
+                float M = kNegInf;
+                #pragma unroll
+                for (int u = 0; u < NW; ++u) M = fmaxf(M, mlw[(u * 16 + r) * 2]);
+                float Lsum = 0.f;
+                float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                #pragma unroll
+                for (int u = 0; u < NW; ++u) {
+                    const float mu = mlw[(u * 16 + r) * 2];
+                    const float sc = (mu == kNegInf) ? 0.f : __builtin_amdgcn_exp2f((mu - M) * c);
+                    Lsum += sc * mlw[(u * 16 + r) * 2 + 1];
+                    const f32x4 a0 = *reinterpret_cast<const f32x4 *>(ow + ((size_t)u * 16 + r) * D + ch * 8);
+                    const f32x4 a1 = *reinterpret_cast<const f32x4 *>(ow + ((size_t)u * 16 + r) * D + ch * 8 + 4);
+                    #pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        acc[e] += sc * a0[e];
+                        acc[4 + e] += sc * a1[e];
+                    }
+                }
+                const float inv = Lsum > 0.f ? 1.f / Lsum : 0.f;
+                bf16x8 o;
+                #pragma unroll
+                for (int e = 0; e < 8; ++e) o[e] = (__bf16)(acc[e] * inv);
+                if (complete) {
+                    const int nd = r / p.G, h = g * p.G + r % p.G;
+                    *reinterpret_cast<bf16x8 *>(p.out + (((size_t)b * p.N + nd) * p.Hq + h) * D + ch * 8) = o;
+                    if (ch == 0 && p.lse)
+                        p.lse[((size_t)b * p.N + nd) * p.Hq + h] = M * p.scale + __builtin_amdgcn_logf(Lsum) * kLn2;
+                } else {
+                    *reinterpret_cast<bf16x8 *>(p.ws_o + ((size_t)slot * p.rows_per_block + r) * D + ch * 8) = o;
+                    if (ch == 0) {
+                        float *pm = p.ws_ml + ((size_t)slot * p.rows_per_block + r) * 2;
+                        pm[0] = (M == kNegInf) ? kNegInf : M * c;
+                        pm[1] = Lsum;
+                    }
+                }
             }
         }
         __syncthreads();                   // the ring is refilled by the next piece
@@ -1118,9 +1342,20 @@ __global__ __launch_bounds__(256) void tree_attention_merge_kernel(AttnParams p,
 
 template <int D, int NW>
 hipError_t launch_dn(const AttnParams &p, hipStream_t s) {
-    hipError_t e = p.small_pages
-        ? launch_kernel(tree_attention_kernel<D, NW, true>, dim3(p.num_wg), dim3(NW * kWave), s, p)
-        : launch_kernel(tree_attention_kernel<D, NW, false>, dim3(p.num_wg), dim3(NW * kWave), s, p);
+    hipError_t e;
+    bool narrow_done = false;
+    if constexpr (NW == 4) {
+        if (p.narrow) {
+            e = p.small_pages
+                ? launch_kernel(tree_attention_kernel<D, NW, true, true>, dim3(p.num_wg), dim3(NW * kWave), s, p)
+                : launch_kernel(tree_attention_kernel<D, NW, false, true>, dim3(p.num_wg), dim3(NW * kWave), s, p);
+            narrow_done = true;
+        }
+    }
+    if (!narrow_done)
+        e = p.small_pages
+            ? launch_kernel(tree_attention_kernel<D, NW, true, false>, dim3(p.num_wg), dim3(NW * kWave), s, p)
+            : launch_kernel(tree_attention_kernel<D, NW, false, false>, dim3(p.num_wg), dim3(NW * kWave), s, p);
     if (e != hipSuccess) return e;
     if (p.num_wg > 1) {
         constexpr int kRowsPerWg = 256 / (D / 8);

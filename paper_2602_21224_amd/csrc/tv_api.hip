@@ -218,6 +218,7 @@ int tree_verify_attention(const uint16_t *q, const uint16_t *k_tree, const uint1
     p.rows_per_block = s.rows_per_block;
     p.setup_tiles = kSetupTiles;
     p.small_pages = P < 1024 / (2 * D) ? 1 : 0;
+    p.narrow = s.rows <= 16 ? 1 : 0;
     p.num_wg = (int)num_wg;
     const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)D);
     p.scale = sc;

@@ -66,6 +66,7 @@ struct AttnParams {
     int B, N, Hq, Hkv, G, P, p_shift, max_pages, num_pages;
     int rows_per_block;          // query rows of one unit (the workgroup's waves x 32)
     int small_pages;             // pages shorter than one 1 KB load block of keys
+    int narrow;                  // units of at most 16 rows: tiles shared out over the waves
     int setup_tiles;             // cost of starting a unit piece, in tiles (work balance)
     int num_wg;
     float scale_log2;            // softmax scale * log2(e)

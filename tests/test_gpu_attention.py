@@ -58,6 +58,8 @@ SMALL = [
     (1, 256, 16, 8, 128, 33, 16, "capped"),     # 512 rows: two row blocks
     (1, 128, 64, 8, 128, 0, 16, "capped"),      # empty prefix, 4 row blocks
     (4, 9, 4, 2, 64, (0, 3), 16, "forest"),     # prefixes shorter than a tile
+    (2, 16, 8, 8, 128, (100, 900), 16, "capped"),   # 16 rows per KV head: the narrow-unit path
+    (3, 5, 6, 2, 128, (0, 300), 2, "forest"),   # 15 narrow rows, G = 3, two-key pages
 ]
 
 
@@ -107,6 +109,7 @@ def test_paper_shape_presets_all_outputs(oracle_mod, name):
     (2, 12, 8, 2, (1500, 3000), 1),    # pages of one key: a 512-key page-id window
     (2, 9, 8, 2, (1600, 2900), 2),     # pages of two keys: 1024-key windows
     (1, 16, 16, 4, 9000, 16),          # 16-key pages: crosses the 8192-key window once
+    (2, 12, 4, 4, (1500, 3000), 1),    # 12 rows per KV head (narrow units) over one-key pages
 ])
 def test_page_id_windows(oracle_mod, B, N, Hq, Hkv, L, P):
     """Pieces whose prefix spans more page ids than the kernel caches at once run in
