@@ -745,24 +745,32 @@ __device__ __forceinline__ void narrow_tile(NarrowState<D> &st, unsigned kbase, 
     constexpr int C = Gm::kChunks;
     constexpr int NKS = D / 32, NDB = D / 16;
     const int g = lane >> 4, i16 = lane & 15;
-    // S^T blocks
+    // S^T blocks; the K reads of block kb + 1 are in flight during block kb's MFMAs
     f32x4 sb[4];
-    #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    u32x4 a[2][NKS];
+    auto read_k = [&](int kb, u32x4 (&dst)[NKS]) {
         const int key = kb * 16 + i16;
         const unsigned row = kbase + key * Gm::kRowBytes;
-        u32x4 a[NKS];
         #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
-            asm volatile("ds_read_b128 %0, %1" : "=v"(a[ks])
+            asm volatile("ds_read_b128 %0, %1" : "=v"(dst[ks])
                          : "v"(row + ((unsigned)((4 * ks + g) ^ swz<C>(key % C)) << 4)));
-        lds_wait<0>();
+    };
+    read_k(0, a[0]);
+    #pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+        if (kb + 1 < 4) {
+            read_k(kb + 1, a[(kb + 1) & 1]);
+            lds_wait<NKS>();
+        } else {
+            lds_wait<0>();
+        }
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-            tie(a[ks]);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[ks]), st.qf[ks],
-                                                          acc, 0, 0, 0);
+            tie(a[kb & 1][ks]);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[kb & 1][ks]),
+                                                          st.qf[ks], acc, 0, 0, 0);
         }
         sb[kb] = acc;
     }
@@ -801,27 +809,39 @@ __device__ __forceinline__ void narrow_tile(NarrowState<D> &st, unsigned kbase, 
             pb[kb >> 1][(kb & 1) * 4 + i] = (__bf16)x;
         }
     st.l_run += ps;
-    // O^T += V^T P^T, two k-steps of 32 keys
-    #pragma unroll
-    for (int kst = 0; kst < 2; ++kst) {
+    // O^T += V^T P^T, two k-steps of 32 keys; step q = kst * NDB + db, its two
+    // transposing reads issued two steps ahead
+    constexpr int NQ = 2 * NDB;
+    u32x2 v[NQ][2];
+    auto read_v = [&](int q) {
+        const int kst = q / NDB, db = q % NDB;
         #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-            u32x2 v[2];
-            #pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const int key = (2 * kst + r) * 16 + 4 * g + (i16 >> 2);
-                const int chunk = 2 * db + ((i16 & 3) >> 1);
-                const unsigned addr = vbase + key * Gm::kRowBytes +
-                                      ((unsigned)(chunk ^ swz<C>(key % C)) << 4) + (i16 & 1) * 8;
-                asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v[r]) : "v"(addr));
-            }
-            lds_wait<0>();
-            tie(v[0]);
-            tie(v[1]);
-            const u32x4 a = {v[0][0], v[0][1], v[1][0], v[1][1]};
-            st.o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), pb[kst],
-                                                               st.o[db], 0, 0, 0);
+        for (int r = 0; r < 2; ++r) {
+            const int key = (2 * kst + r) * 16 + 4 * g + (i16 >> 2);
+            const int chunk = 2 * db + ((i16 & 3) >> 1);
+            const unsigned addr = vbase + key * Gm::kRowBytes +
+                                  ((unsigned)(chunk ^ swz<C>(key % C)) << 4) + (i16 & 1) * 8;
+            asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v[q][r]) : "v"(addr));
         }
+    };
+    read_v(0);
+    read_v(1);
+    #pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        if (q + 2 < NQ) {
+            read_v(q + 2);
+            lds_wait<4>();
+        } else if (q + 1 < NQ) {
+            lds_wait<2>();
+        } else {
+            lds_wait<0>();
+        }
+        tie(v[q][0]);
+        tie(v[q][1]);
+        const int kst = q / NDB, db = q % NDB;
+        const u32x4 av = {v[q][0][0], v[q][0][1], v[q][1][0], v[q][1][1]};
+        st.o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), pb[kst],
+                                                           st.o[db], 0, 0, 0);
     }
 }
 
