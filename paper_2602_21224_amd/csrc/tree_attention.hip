@@ -914,6 +914,16 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         // r is virtual tile C + r
         const int v_end = min(C + ulen, off + (end - pos));
         const int unit_real_start = pos - off + C;    // share coordinate of real tile 0
+        const int t0 = max(off - C, 0);
+        // Page ids of the first four tiles (scalar loads): for narrow units first
+        // of all, so that their latency overlaps the rest of the set-up; for the
+        // others after the parent links (holding them that long costs the
+        // eight-wave kernel spills). Later sub-ranges fetch their own.
+        int ids[4][Issue::kLoadsPerWave];
+        if constexpr (NARROW) {
+            #pragma unroll
+            for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, t0 + i, wave_u, ids[i]);
+        }
         if (pos == start && tid == 0) {
             // the merge kernel's entry for this workgroup: the split unit whose
             // last piece is this share's first, if any
@@ -924,7 +934,6 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
                      : i32x4{-1, 0, 0, 0};
         }
         pos += v_end - off;
-        const int t0 = max(off - C, 0);
         const int t_end = v_end - C;
         if (t_end <= t0) continue;                    // only set-up tiles of this unit
         const bool complete = (t0 == 0 && t_end == ulen);
@@ -937,12 +946,10 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
         int par_pre = -1;
         if (need_anc && wave_u == 0 && p.N <= kWave && lane < p.N)
             par_pre = p.parent[(size_t)b * p.N + lane];
-
-        // Page ids of the first four tiles (scalar loads), ahead of the Q loads
-        // so that their latency overlaps them; later sub-ranges fetch their own.
-        int ids[4][Issue::kLoadsPerWave];
-        #pragma unroll
-        for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, t0 + i, wave_u, ids[i]);
+        if constexpr (!NARROW) {
+            #pragma unroll
+            for (int i = 0; i < 4; ++i) ld.fetch_pages(p, b, t0 + i, wave_u, ids[i]);
+        }
 
         // ---- this wave's 32 query rows: Q fragments stay in registers. A row
         // past the unit's last one loads the unit's first row instead (rows are
@@ -1029,25 +1036,41 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             };
             ld.set_unit(p, b, g, L, ntp, nodes);
             {
+                // narrow units: full prefix tiles take the fast address path here too
                 typename Issue::Blocks b0, b1;
-                #pragma unroll
-                for (int k = 0; k < LPT; ++k) pk[k] = ids[0][k];
-                b0 = blocks_of(0);
-                #pragma unroll
-                for (int k = 0; k < LPT; ++k) pk[k] = ids[1][k];
-                b1 = blocks_of(1);
-                #pragma unroll
-                for (int k = 0; k < LPT; ++k) pk[k] = ids[2][k];
-                bk = blocks_of(2);             // K_2 now, V_2 in period 0 (narrow: now)
-                // issue order K_0, V_0, K_1, V_1, K_2 (, V_2) (the waits below count on it)
-                issue_half(0, false, b0);
-                issue_half(0, true, b0);
-                if (T > 1) {
-                    issue_half(1, false, b1);
-                    issue_half(1, true, b1);
+                unsigned long long f0 = 0, f1 = 0;
+                const bool fa0 = NARROW && !SMALL && ld.fast_offset(p, ta, wave_u, ids[0][0], f0);
+                const bool fa1 = NARROW && !SMALL && T > 1 && ld.fast_offset(p, ta + 1, wave_u, ids[1][0], f1);
+                fast = NARROW && !SMALL && T > 2 && ld.fast_offset(p, ta + 2, wave_u, ids[2][0], foff);
+                if (!fa0) {
+                    #pragma unroll
+                    for (int k = 0; k < LPT; ++k) pk[k] = ids[0][k];
+                    b0 = blocks_of(0);
                 }
-                if (T > 2) issue_half(2, false, bk);
-                if (NARROW && T > 2) issue_half(2, true, bk);
+                if (T > 1 && !fa1) {
+                    #pragma unroll
+                    for (int k = 0; k < LPT; ++k) pk[k] = ids[1][k];
+                    b1 = blocks_of(1);
+                }
+                if (T > 2 && !fast) {
+                    #pragma unroll
+                    for (int k = 0; k < LPT; ++k) pk[k] = ids[2][k];
+                    bk = blocks_of(2);         // K_2 now, V_2 in period 0 (narrow: now)
+                }
+                auto issue_pro = [&](int i, bool is_v, bool fa, unsigned long long fo,
+                                     const typename Issue::Blocks &bl) {
+                    if (fa) ld.issue_fast(fo, is_v, (ta + i) & (NS - 1), wave_u);
+                    else issue_half(i, is_v, bl);
+                };
+                // issue order K_0, V_0, K_1, V_1, K_2 (, V_2) (the waits below count on it)
+                issue_pro(0, false, fa0, f0, b0);
+                issue_pro(0, true, fa0, f0, b0);
+                if (T > 1) {
+                    issue_pro(1, false, fa1, f1, b1);
+                    issue_pro(1, true, fa1, f1, b1);
+                }
+                if (T > 2) issue_pro(2, false, fast, foff, bk);
+                if (NARROW && T > 2) issue_pro(2, true, fast, foff, bk);
                 #pragma unroll
                 for (int k = 0; k < LPT; ++k) pk[k] = ids[3][k];
             }
