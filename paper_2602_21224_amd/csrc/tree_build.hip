@@ -101,11 +101,16 @@ __device__ __forceinline__ unsigned long long wave_max64(unsigned long long v) {
                   umax64(readlane64(v, 47), readlane64(v, 63)));
 }
 
-// Largest 32-bit value over the wave.
+// Largest 32-bit value over the wave: a scan of per-row maxima by DPP row
+// shifts, then the four rows' last lanes (no LDS).
 __device__ __forceinline__ unsigned int wave_max32(unsigned int v) {
-    #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = max(v, (unsigned int)__shfl_xor((int)v, off));
-    return v;
+    v = max(v, (unsigned int)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x111, 0xF, 0xF, false));
+    v = max(v, (unsigned int)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x112, 0xF, 0xF, false));
+    v = max(v, (unsigned int)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x114, 0xF, 0xF, false));
+    v = max(v, (unsigned int)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x118, 0xF, 0xF, false));
+    // lane 15 of every row now holds its row's maximum
+    return max(max((unsigned int)__builtin_amdgcn_readlane((int)v, 15), (unsigned int)__builtin_amdgcn_readlane((int)v, 31)),
+               max((unsigned int)__builtin_amdgcn_readlane((int)v, 47), (unsigned int)__builtin_amdgcn_readlane((int)v, 63)));
 }
 
 // A wave's top-k list, distributed over lanes: lane j < k holds the (j+1)-th
@@ -188,12 +193,15 @@ __device__ __forceinline__ void fold_chunk(const float (&x)[U], Id id, int k, in
         os.merge(m, sum);
     }
     // k-th largest lane maximum (ties may remove two lanes in one round: the
-    // floor only gets lower, never wrong)
-    unsigned int floor_key = 0u;
-    for (int r = 0; r < k; ++r) {
-        const unsigned int mx = wave_max32(kmax);
-        if (kmax == mx) kmax = 0u;
-        floor_key = mx;
+    // floor only gets lower, never wrong); once the wave's list is full, its
+    // k-th key is a floor already and the rounds are skipped
+    unsigned int floor_key = (unsigned int)(tk.thr >> 32);
+    if (floor_key == 0u) {
+        for (int r = 0; r < k; ++r) {
+            const unsigned int mx = wave_max32(kmax);
+            if (kmax == mx) kmax = 0u;
+            floor_key = mx;
+        }
     }
     #pragma unroll
     for (int u = 0; u < U; ++u) {
