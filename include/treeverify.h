@@ -363,8 +363,9 @@ TV_API int tree_build(const float *logits, const int32_t *root_token, const uint
  *   workspace    >= tv_lm_head_workspace_size(B, N, V, d) bytes of device
  *                memory, 8-byte aligned; contents on entry do not matter.
  * Supported: 0 <= B <= 65535, 1 <= N <= 256, 1 <= V <= 2^31 - 257, d a
- * multiple of 32 (>= 32), and at most 2^31 - 1 workgroups (V/256 x B N/256,
- * rounded up).
+ * multiple of 64 (>= 64; the weight streams in 64-deep units of whole
+ * 128-byte lines), and at most 2^31 - 1 workgroups (V/256 x B N/256,
+ * rounded up). Other shapes return TV_ERR_SHAPE.
  * ------------------------------------------------------------------------ */
 TV_API size_t tv_lm_head_workspace_size(int B, int N, int V, int d);
 

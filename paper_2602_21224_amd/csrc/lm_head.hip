@@ -16,20 +16,25 @@
 //     Eight waves (two per SIMD, so one wave's waits are covered by the
 //     other's matrix work) in a 2 x 4 arrangement, each accumulating a
 //     128 x 64 block in 8 v_mfma_f32_32x32x16_bf16 accumulators.
-//   * Both operands are K-contiguous (W is [V, d], hidden is [R, d]), so both
-//     stream into LDS the same way: global_load_lds_dwordx4 into a 4-stage
-//     ring of 32-deep K slices. The four 16-byte chunks of each 64-byte row
-//     slice are XOR-swizzled by bits 2-3 of the row, so the operand reads
-//     (16 rows at one chunk per LDS pass) are free of bank conflicts.
-//   * The reads of the next K step's operands and the loads of the slice
-//     four ahead are interleaved one by one with the current step's MFMAs
-//     (pinned by sched_barrier), and the ring hand-off (s_waitcnt vmcnt +
-//     s_barrier) sits a few MFMAs into a slice's second K step, after this
-//     wave's last read of the slice whose stage is refilled next: three
-//     slices are in flight while one is computed.
-//   * Workgroup order: ids are dispatched round-robin over the 8 XCDs, so
-//     they are mapped such that the row blocks of one vocabulary tile run back
-//     to back on one XCD and share its L2 copy of that weight tile.
+//   * Both operands are K-contiguous (W is [V, d], hidden is [R, d]) and both
+//     stream into LDS through global_load_lds_dwordx4, each in its own ring.
+//     The weight, which comes from HBM and whose load latency bounds the
+//     stream, moves in 64-deep units (each row's 128 bytes = whole cache
+//     lines; a 1 KB load covers 8 rows) through a 3-stage ring, two units in
+//     flight; the hidden rows, re-read from L2, move in 32-deep slices (16
+//     rows x 64 bytes per load) through a 4-stage ring, issued 1.5 units ahead.
+//     Together 160 KB: the whole LDS. The 16-byte chunks of each row are
+//     XOR-swizzled by the row index so the operand reads (16 rows at one chunk
+//     per LDS pass) are free of bank conflicts.
+//   * Each 16-deep K step's 8 MFMAs carry, one by one, the next step's 6
+//     fragment reads; two ring hand-offs per unit (s_waitcnt vmcnt +
+//     s_barrier), a few MFMAs into steps 1 and 3 after this wave's last read of
+//     the stages refilled next, are followed by the refill loads.
+//   * The four row blocks of one vocabulary tile run together on one XCD and
+//     share its L2 copy of the weight tile; each takes the units of every
+//     aligned group of four in an order rotated by its row block, so the four
+//     ask HBM for different lines at any time (more distinct bytes in flight)
+//     and find the others' lines in L2 a few units later.
 //   * Epilogue: each lane folds its 64 values per row into a key, lanes l and
 //     l ^ 32 combine, the two waves of a row block combine through LDS, and a
 //     64-bit atomic maximum per (row, vocabulary tile) merges the tiles into
@@ -48,22 +53,27 @@ constexpr int kWaves = 8;                              // two per SIMD
 constexpr int kLmThreads = kWaves * kWave;
 constexpr int kTileM = 256;                            // vocabulary entries per workgroup
 constexpr int kTileN = 256;                            // hidden rows per workgroup
-constexpr int kBK = 32;                                // K depth of one ring stage
-constexpr int kStages = 4;                             // a power of two
-constexpr int kSliceRow = kBK * 2;                     // bytes of one row's K slice
-constexpr int kOperandBytes = kTileM * kSliceRow;      // 16 KB per operand per stage
-constexpr int kStageBytes = 2 * kOperandBytes;         // W slice, then hidden slice
-constexpr int kLoads = kOperandBytes / (kLmThreads * 16);   // 16-byte loads per operand per thread
+constexpr int kUnitK = 64;                             // K depth of one weight unit
+constexpr int kWRow = kUnitK * 2;                      // bytes of one weight row's unit (128)
+constexpr int kWUnitBytes = kTileM * kWRow;            // 32 KB
+constexpr int kWStages = 3;
+constexpr int kHK = 32;                                // K depth of one hidden slice
+constexpr int kHRow = kHK * 2;                         // bytes of one hidden row's slice (64)
+constexpr int kHSliceBytes = kTileN * kHRow;           // 16 KB
+constexpr int kHStages = 4;
+constexpr int kWLoads = kWUnitBytes / (kLmThreads * 16);    // 1 KB loads per thread per unit (4)
+constexpr int kHLoads = kHSliceBytes / (kLmThreads * 16);   // per slice (2)
 constexpr int kWaveM = 128;                            // per-wave block: 2 waves along M
 constexpr int kWaveN = kTileN / (kWaves / 2);
 constexpr int kFragM = kWaveM / 32, kFragN = kWaveN / 32;
 constexpr int kReads = kFragM + kFragN;                // fragment reads per K step
 constexpr int kSteps = kFragM * kFragN;                // MFMAs per K step
-static_assert(kTileM == kTileN, "both operands share one slice layout");
-static_assert(kLoads * kWaves == 16, "one 1 KB block per load instruction: 16 blocks per operand");
+constexpr int kPre = 2;                                // MFMAs before a hand-off
+static_assert(kWLoads * kWaves * 8 == kTileM && kHLoads * kWaves * 16 == kTileN, "load blocks");
+static_assert(kWStages * kWUnitBytes + kHStages * kHSliceBytes <= 160 * 1024, "LDS");
 
-__shared__ __attribute__((aligned(1024))) unsigned char g_lm_ring[kStages * kStageBytes];
-__shared__ unsigned long long g_lm_keys[kWaves / 2][kWaveN];
+__shared__ __attribute__((aligned(1024))) unsigned char g_lm_w[kWStages * kWUnitBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char g_lm_h[kHStages * kHSliceBytes];
 
 __device__ __forceinline__ unsigned lds_addr(const void *p) {
     return (unsigned)(size_t)(const LDS_AS void *)p;
@@ -81,6 +91,13 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit field");
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ void wait_vmcnt_rt(int n) {     // n in {0, 2, 4, 8}
+    if (n >= 8) wait_vmcnt<8>();
+    else if (n >= 4) wait_vmcnt<4>();
+    else if (n >= 2) wait_vmcnt<2>();
+    else wait_vmcnt<0>();
 }
 
 __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
@@ -103,6 +120,7 @@ __global__ void lm_keys_clear_kernel(unsigned long long *__restrict__ keys, int 
 }
 
 // grid: kNumXcd * ceil(vtiles / kNumXcd) * rblocks workgroups of kLmThreads threads.
+// d is a multiple of kUnitK.
 __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
     const uint16_t *__restrict__ hidden, const uint16_t *__restrict__ w, int R, int V, int d,
     int vtiles, int rblocks, unsigned long long *__restrict__ keys) {
@@ -115,34 +133,57 @@ __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid & (kWave - 1);
+    const int U = d / kUnitK;                    // weight units; hidden slices: 2 U
 
-    // Slice loads: instruction i of wave w fills 1 KB block (4w + i) of an
-    // operand = rows 16 (4w + i) .. +15; lane p writes row p / 4, position
-    // p % 4, which holds chunk (p % 4) ^ ((row >> 2) & 3). Rows past the end
-    // of W or hidden read the last row (finite data; results are discarded).
-    const char *asrc[kLoads], *bsrc[kLoads];
+    // Weight loads: instruction i of wave w fills 1 KB block (4w + i) of a
+    // unit = rows 8 (4w + i) .. +7; lane p writes row p / 8, position p % 8,
+    // which holds chunk (p % 8) ^ ((row >> 1) & 7). Hidden loads: instruction
+    // i fills block (2w + i) of a slice = rows 16 (2w + i) .. +15; lane p
+    // writes row p / 4, position p % 4 = chunk (p % 4) ^ ((row >> 2) & 3).
+    // Rows past the end of W or hidden read the last row (finite data; the
+    // results are discarded).
+    const char *wsrc[kWLoads], *hsrc[kHLoads];
     {
-        const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
         #pragma unroll
-        for (int i = 0; i < kLoads; ++i) {
-            const int row = (wave * kLoads + i) * 16 + (lane >> 2);
-            const int vr = min(v0 + row, V - 1);
-            const int hr = min(r0 + row, R - 1);
-            asrc[i] = reinterpret_cast<const char *>(w + (size_t)vr * d) + chunk * 16;
-            bsrc[i] = reinterpret_cast<const char *>(hidden + (size_t)hr * d) + chunk * 16;
+        for (int i = 0; i < kWLoads; ++i) {
+            const int row = (wave * kWLoads + i) * 8 + (lane >> 3);
+            const int chunk = (lane & 7) ^ ((row >> 1) & 7);
+            wsrc[i] = reinterpret_cast<const char *>(w + (size_t)min(v0 + row, V - 1) * d) + chunk * 16;
+        }
+        #pragma unroll
+        for (int i = 0; i < kHLoads; ++i) {
+            const int row = (wave * kHLoads + i) * 16 + (lane >> 2);
+            const int chunk = (lane & 3) ^ ((row >> 2) & 3);
+            hsrc[i] = reinterpret_cast<const char *>(hidden + (size_t)min(r0 + row, R - 1) * d) + chunk * 16;
         }
     }
-    const int T = d / kBK;
+    // Unit order: inside every complete aligned group of four, rotated by the
+    // row block (a permutation of 0 .. U - 1).
+    const int U4 = U & ~3;
+    auto unit_of = [&](int u) { return u < U4 ? (u & ~3) | ((u + rb) & 3) : u; };
+    // Load i of a weight unit / hidden slice: LDS stage offset, K byte offset.
+    auto issue_w = [&](unsigned stage_off, size_t koff, int i) {
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(wsrc[i] + koff),
+                                         (LDS_AS void *)(g_lm_w + stage_off + (wave * kWLoads + i) * 1024),
+                                         16, 0, 0);
+    };
+    auto issue_h = [&](unsigned stage_off, size_t koff, int i) {
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(hsrc[i] + koff),
+                                         (LDS_AS void *)(g_lm_h + stage_off + (wave * kHLoads + i) * 1024),
+                                         16, 0, 0);
+    };
 
     // Operand fragments of v_mfma_f32_32x32x16_bf16: lane l reads row l % 32
-    // of a 32-row block, K elements 8 (l / 32) .. +7 of the 16-deep step, i.e.
-    // chunk 2 s + l / 32 of the slice for step s; with the swizzle the chunk's
-    // position is (2 s + l / 32) ^ ((l >> 2) & 3) = (base position) ^ 2 s.
+    // of a 32-row block, K elements 8 (l / 32) .. +7 of the 16-deep step.
+    // Step s (0..3) of a unit is weight chunk 2 s + l / 32, whose position is
+    // (l / 32) ^ ((row >> 1) & 7) ^ 2 s, and hidden slice s / 2, chunk
+    // 2 (s % 2) + l / 32 at position (l / 32) ^ ((row >> 2) & 3) ^ 2 (s % 2).
     const int wm = wave & 1, wn = wave >> 1;
-    const unsigned ring = lds_addr(g_lm_ring);
-    const unsigned swz = (unsigned)((((lane >> 5) ^ (lane >> 2)) & 3) << 4);
-    const unsigned a_lane = (unsigned)((wm * kWaveM + (lane & 31)) * kSliceRow) + swz;
-    const unsigned b_lane = (unsigned)(kOperandBytes + (wn * kWaveN + (lane & 31)) * kSliceRow) + swz;
+    const unsigned wring = lds_addr(g_lm_w), hring = lds_addr(g_lm_h);
+    const unsigned a_lane = wring + (unsigned)((wm * kWaveM + (lane & 31)) * kWRow) +
+                            (unsigned)((((lane >> 5) ^ (lane >> 1)) & 7) << 4);
+    const unsigned b_lane = hring + (unsigned)((wn * kWaveN + (lane & 31)) * kHRow) +
+                            (unsigned)((((lane >> 5) ^ (lane >> 2)) & 3) << 4);
 
     f32x16 acc[kFragM][kFragN];
     #pragma unroll
@@ -153,16 +194,13 @@ __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
             for (int e = 0; e < 16; ++e) acc[m][n][e] = 0.f;
     u32x4 fa[2][kFragM], fb[2][kFragN];
 
-    auto frag_addr = [&](int stage, int s, unsigned lane_off) {
-        return (ring + (unsigned)(stage * kStageBytes) + lane_off) ^ ((unsigned)s << 5);
-    };
-    // Read q (0..7) of a fragment set: A fragments 0..3, then B fragments 0..3.
+    // Read q (0..5) of a fragment set: A fragments 0..3, then B fragments 0..1.
     auto read_q = [&](int set, unsigned aa, unsigned ba, int q) {
         if (q < kFragM)
-            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(fa[set][q]) : "v"(aa), "i"(q * 32 * kSliceRow));
+            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(fa[set][q]) : "v"(aa), "i"(q * 32 * kWRow));
         else
             asm volatile("ds_read_b128 %0, %1 offset:%2"
-                         : "=v"(fb[set][q - kFragM]) : "v"(ba), "i"((q - kFragM) * 32 * kSliceRow));
+                         : "=v"(fb[set][q - kFragM]) : "v"(ba), "i"((q - kFragM) * 32 * kHRow));
     };
     auto ready = [&](int set) {             // after lds_wait_all: the set is in registers
         #pragma unroll
@@ -176,98 +214,133 @@ __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
             __builtin_bit_cast(bf16x8, fa[set][m]), __builtin_bit_cast(bf16x8, fb[set][n]),
             acc[m][n], 0, 0, 0);
     };
-    auto issue_load = [&](int t, int i) {     // load i (0 .. 2 kLoads - 1) of slice t
-        unsigned char *st = g_lm_ring + (t & (kStages - 1)) * kStageBytes;
-        const size_t koff = (size_t)t * kSliceRow;
-        if (i < kLoads)
-            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(asrc[i] + koff),
-                                             (LDS_AS void *)(st + (wave * kLoads + i) * 1024), 16, 0, 0);
-        else
-            __builtin_amdgcn_global_load_lds((const GLOBAL_AS void *)(bsrc[i - kLoads] + koff),
-                                             (LDS_AS void *)(st + kOperandBytes + (wave * kLoads + i - kLoads) * 1024),
-                                             16, 0, 0);
-    };
 
-    // One K slice j. Step (j, 0) is in fragment set 0 (reads issued earlier).
-    // First half: its 16 MFMAs with the reads of step (j, 1) into set 1 between
-    // them. Second half: set 1's MFMAs; after the first four, the ring hand-off
-    // (slice j + 1 landed everywhere; every wave is done with slice j, whose
-    // stage slice j + 4 takes), then the loads of slice j + 4 and the reads of
-    // step (j + 1, 0) between the rest. sched_barrier pins the interleaving.
-    auto slice = [&](int j, bool more, bool load4, auto wait_next) {
-        constexpr int kPre = kSteps / 4;                 // MFMAs before the hand-off
-        constexpr int kOps = 2 * kLoads + kReads;        // loads, then reads, after it
-        constexpr int kPer = (kOps + kSteps - kPre - 1) / (kSteps - kPre);
-        lds_wait_all();
-        ready(0);
-        {
-            const unsigned aa = frag_addr(j & (kStages - 1), 1, a_lane);
-            const unsigned ba = frag_addr(j & (kStages - 1), 1, b_lane);
-            #pragma unroll
-            for (int q = 0; q < kSteps; ++q) {
-                mfma_q(0, q);
-                if (q < kReads) read_q(1, aa, ba, q);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-        lds_wait_all();
-        ready(1);
+    // Issue order, the same in the prologue and the steady state: hand-off A
+    // of unit u (in step 1) issues hidden slice 2u + 4; hand-off B (in step 3)
+    // issues weight unit u + 3, then hidden slice 2u + 5. Stages: weight unit
+    // x in x % 3, hidden slice x in x % 4. The prologue plays hand-offs
+    // B(-3), A(-2), B(-2), A(-1), B(-1).
+    {
+        const size_t k0 = (size_t)unit_of(0) * kWRow, k1 = (size_t)unit_of(1) * kWRow;
         #pragma unroll
-        for (int q = 0; q < kPre; ++q) {
-            mfma_q(1, q);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        if (more) {
-            wait_next();
-            __builtin_amdgcn_s_barrier();
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        const unsigned aa = frag_addr((j + 1) & (kStages - 1), 0, a_lane);
-        const unsigned ba = frag_addr((j + 1) & (kStages - 1), 0, b_lane);
+        for (int i = 0; i < kWLoads; ++i) issue_w(0, k0, i);                          // W0
         #pragma unroll
-        for (int q = kPre; q < kSteps; ++q) {
-            mfma_q(1, q);
+        for (int i = 0; i < kHLoads; ++i) issue_h(0, k0, i);                          // H0
+        if (U >= 2)
             #pragma unroll
-            for (int u = 0; u < kPer; ++u) {
-                const int op = (q - kPre) * kPer + u;
-                if (op < 2 * kLoads) {
-                    if (load4) issue_load(j + 4, op);
-                } else if (op < kOps) {
-                    if (more) read_q(0, aa, ba, op - 2 * kLoads);
+            for (int i = 0; i < kWLoads; ++i) issue_w(kWUnitBytes, k1, i);            // W1
+        #pragma unroll
+        for (int i = 0; i < kHLoads; ++i) issue_h(kHSliceBytes, k0 + kHRow, i);       // H1
+        if (U >= 2)
+            #pragma unroll
+            for (int i = 0; i < kHLoads; ++i) issue_h(2 * kHSliceBytes, k1, i);       // H2
+        if (U >= 3) {
+            const size_t k2 = (size_t)unit_of(2) * kWRow;
+            #pragma unroll
+            for (int i = 0; i < kWLoads; ++i) issue_w(2 * kWUnitBytes, k2, i);        // W2
+        }
+        if (U >= 2)
+            #pragma unroll
+            for (int i = 0; i < kHLoads; ++i) issue_h(3 * kHSliceBytes, k1 + kHRow, i);   // H3
+        // Unit 0 needs W0 and H0; what came after may stay in flight.
+        if (U >= 3) wait_vmcnt<kHLoads + kWLoads + 2 * kHLoads + kWLoads>();
+        else if (U >= 2) wait_vmcnt<kHLoads + kWLoads + 2 * kHLoads>();
+        else wait_vmcnt<kHLoads>();
+    }
+    __builtin_amdgcn_s_barrier();
+    #pragma unroll
+    for (int q = 0; q < kReads; ++q) read_q(0, a_lane, b_lane, q);
+
+    // One unit u (4 steps of 16). Step s's fragments are in set s & 1. Steps 0
+    // and 2: 8 MFMAs with the next step's 6 reads between them. Steps 1 and 3:
+    // kPre MFMAs, the hand-off (the data of the next reads landed everywhere;
+    // every wave is done with the stages refilled now), then the remaining
+    // MFMAs carrying the hand-off's loads and then the next step's reads.
+    // sched_barrier pins the interleaving. kSteady: u + 3 < U, so every load
+    // of the hand-offs exists and the waits are constant.
+    int wst = 0;                                      // weight stage of unit u
+    auto unit = [&](int u, auto steady_c) {
+        constexpr bool kSteady = decltype(steady_c)::value;
+        const unsigned wcur = (unsigned)wst * kWUnitBytes;
+        const unsigned wnxt = (unsigned)(wst == kWStages - 1 ? 0 : wst + 1) * kWUnitBytes;
+        const unsigned hcur = (unsigned)(u & 1) * 2 * kHSliceBytes;     // stage of slice 2u
+        const unsigned a0 = a_lane + wcur, a1 = a_lane + wnxt;
+        const unsigned b0 = b_lane + hcur, b1 = b_lane + (hcur ^ 2 * kHSliceBytes);
+        const size_t kw = (size_t)unit_of(u + 3) * kWRow;              // weight unit u + 3
+        const size_t kh = (size_t)unit_of(u + 2) * kWRow;              // hidden slices 2u + 4, 2u + 5
+        const bool has_w = kSteady || u + 3 < U;
+        const bool has_h = kSteady || u + 2 < U;
+        const bool has_next = kSteady || u + 1 < U;
+
+        auto step = [&](auto sc) {
+            constexpr int s = decltype(sc)::value;
+            constexpr int set = s & 1;
+            const unsigned aa = s == 3 ? a1 : a0 ^ ((unsigned)(s + 1) << 5);
+            const unsigned ba = s == 3 ? b1
+                                       : (b0 + (unsigned)(((s + 1) >> 1) * kHSliceBytes)) ^
+                                             ((unsigned)((s + 1) & 1) << 5);
+            lds_wait_all();
+            ready(set);
+            if constexpr (s == 0 || s == 2) {
+                #pragma unroll
+                for (int q = 0; q < kSteps; ++q) {
+                    mfma_q(set, q);
+                    if (q < kReads) read_q(set ^ 1, aa, ba, q);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else {
+                constexpr int kLoadsHere = s == 1 ? kHLoads : kWLoads + kHLoads;
+                constexpr int kOps = kLoadsHere + kReads;
+                constexpr int kPer = (kOps + kSteps - kPre - 1) / (kSteps - kPre);
+                const bool next = s == 1 || has_next;
+                #pragma unroll
+                for (int q = 0; q < kPre; ++q) {
+                    mfma_q(set, q);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                if (next) {
+                    // loads issued after the newest one the next reads need
+                    if constexpr (kSteady) {
+                        wait_vmcnt<2 * kWLoads>();
+                    } else if constexpr (s == 1) {   // hidden slice 2u + 1 (from B(u - 2))
+                        wait_vmcnt_rt((u + 1 < U ? 4 : 0) + (u + 2 < U ? 4 : 0));
+                    } else {                         // unit u + 1 (B(u - 2)), slice 2u + 2 (A(u - 1))
+                        wait_vmcnt_rt((u + 2 < U ? 6 : 0) + (u + 1 < U ? 2 : 0));
+                    }
+                    __builtin_amdgcn_s_barrier();
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                #pragma unroll
+                for (int q = kPre; q < kSteps; ++q) {
+                    mfma_q(set, q);
+                    #pragma unroll
+                    for (int x = 0; x < kPer; ++x) {
+                        const int op = (q - kPre) * kPer + x;
+                        if (op < kLoadsHere) {
+                            if (s == 1) {
+                                if (has_h) issue_h(hcur, kh, op);                       // slice 2u + 4
+                            } else if (op < kWLoads) {
+                                if (has_w) issue_w(wcur, kw, op);                       // unit u + 3
+                            } else if (has_h) {
+                                issue_h(hcur + kHSliceBytes, kh + kHRow, op - kWLoads); // slice 2u + 5
+                            }
+                        } else if (op < kOps) {
+                            if (next) read_q(set ^ 1, aa, ba, op - kLoadsHere);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
-            __builtin_amdgcn_sched_barrier(0);
-        }
+        };
+        step(std::integral_constant<int, 0>());
+        step(std::integral_constant<int, 1>());
+        step(std::integral_constant<int, 2>());
+        step(std::integral_constant<int, 3>());
+        wst = wst == kWStages - 1 ? 0 : wst + 1;
     };
-
-    // Slices 0..3 in flight; wait for slice 0 (later slices may stay pending).
-    #pragma unroll
-    for (int t = 0; t < kStages; ++t)
-        if (t < T)
-            #pragma unroll
-            for (int i = 0; i < 2 * kLoads; ++i) issue_load(t, i);
-    if (T > 3) wait_vmcnt<6 * kLoads>();
-    else if (T > 2) wait_vmcnt<4 * kLoads>();
-    else if (T > 1) wait_vmcnt<2 * kLoads>();
-    else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    {
-        const unsigned aa = frag_addr(0, 0, a_lane), ba = frag_addr(0, 0, b_lane);
-        #pragma unroll
-        for (int q = 0; q < kReads; ++q) read_q(0, aa, ba, q);
-    }
-    // Steady state: at the hand-off of slice j, slices j + 2 and j + 3 may
-    // still be in flight (2 x 2 kLoads loads of this thread).
-    int j = 0;
-    for (; j + 4 < T; ++j) slice(j, true, true, [] { wait_vmcnt<4 * kLoads>(); });
-    for (; j < T; ++j) {
-        const int after = T - 2 - j;          // slices issued after j + 1
-        slice(j, j + 1 < T, false, [&] {
-            if (after >= 2) wait_vmcnt<4 * kLoads>();
-            else if (after == 1) wait_vmcnt<2 * kLoads>();
-            else wait_vmcnt<0>();
-        });
-    }
+    int u = 0;
+    for (; u + 3 < U; ++u) unit(u, std::true_type());
+    for (; u < U; ++u) unit(u, std::false_type());
 
     // Epilogue. acc[m][n][e] of lane l: hidden row 32 n + l % 32 of the wave's
     // block, vocabulary entry 32 m + 8 (e / 4) + 4 (l / 32) + e % 4.
@@ -286,16 +359,20 @@ __global__ __launch_bounds__(kLmThreads, 1) void lm_head_argmax_kernel(
             }
         best[n] = halves_max64(b);
     }
+    // The keys of the two M-waves meet in LDS (the hidden ring, free once
+    // every wave is past its last fragment read).
+    unsigned long long *kx = reinterpret_cast<unsigned long long *>(g_lm_h);
+    __syncthreads();
     if (wm == 1 && lane < 32) {
         #pragma unroll
-        for (int n = 0; n < kFragN; ++n) g_lm_keys[wn][32 * n + lane] = best[n];
+        for (int n = 0; n < kFragN; ++n) kx[wn * kWaveN + 32 * n + lane] = best[n];
     }
     __syncthreads();
     if (wm == 0 && lane < 32) {
         #pragma unroll
         for (int n = 0; n < kFragN; ++n) {
             const int row = r0 + wn * kWaveN + 32 * n + lane;
-            if (row < R) atomicMax(keys + row, umax64(best[n], g_lm_keys[wn][32 * n + lane]));
+            if (row < R) atomicMax(keys + row, umax64(best[n], kx[wn * kWaveN + 32 * n + lane]));
         }
     }
 }

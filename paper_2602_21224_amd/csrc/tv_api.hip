@@ -398,7 +398,7 @@ int tree_resample(const float *logits, const int32_t *bonus_token, const int32_t
 static bool lm_head_shape_ok(int B, int N, int V, int d) {
     // V: vocabulary ids of a tile's rows (v0 + 0..255) must fit an int
     if (B < 0 || B > 65535 || N < 1 || N > tv::kMaxNodes || V < 1 || V > 0x7FFFFFFF - 256 ||
-        d < 32 || d % 32 != 0)
+        d < 64 || d % 64 != 0)
         return false;
     const long long rblocks = ((long long)B * N + 255) / 256;
     const long long groups = ((long long)tv::lm_head_vocab_tiles(V) + 7) / 8 * 8 * rblocks;

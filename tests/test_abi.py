@@ -174,7 +174,7 @@ def test_lm_head_argument_checks(lib):
     assert lm(B=0) == 0
     assert lm(hidden=NULL) == -1 and lm(w=NULL) == -1 and lm(bonus=NULL) == -1
     assert lm(ws=NULL) == -1
-    assert lm(d=0) == -2 and lm(d=48) == -2 and lm(d=16) == -2          # d: multiple of 32
+    assert lm(d=0) == -2 and lm(d=48) == -2 and lm(d=32) == -2 and lm(d=96) == -2   # d: multiple of 64
     assert lm(V=0) == -2 and lm(N=257) == -2 and lm(B=65536) == -2
     assert lm(B=65535, N=256, V=(1 << 31) - 257) == -2                  # grid above 2^31 - 1
     assert lm(B=1, N=1, V=(1 << 31) - 256) == -2                        # tile ids past 2^31 - 1

@@ -78,12 +78,13 @@ def check_accept(oracle_mod, x, got, label):
 CASES = [
     # (B, N, V, d, num_nodes)
     (2, 16, 1000, 256, None),
-    (3, 37, 1000, 96, [37, 5, 20]),      # ragged rows and vocabulary, three K slices
-    (1, 8, 257, 32, None),               # one K slice, one entry past a vocabulary tile
-    (2, 4, 300, 64, None),               # two K slices
+    (3, 37, 1000, 192, [37, 5, 20]),     # ragged rows and vocabulary, three K units
+    (1, 8, 257, 64, None),               # one K unit, one entry past a vocabulary tile
+    (2, 4, 300, 128, None),              # two K units
     (1, 3, 1, 128, None),                # a single vocabulary entry
     (4, 64, 20000, 1024, None),          # full row tile, many vocabulary tiles
     (5, 64, 3000, 512, [64, 0, 17, 64, 1]),   # row tiles split across sequences, empty ones
+    (6, 64, 900, 320, None),             # two row blocks, five K units: a rotated group of four + one
 ]
 
 
