@@ -39,6 +39,25 @@ struct TbPart {
     unsigned long long key[kTbMaxK];
 };
 
+// The frontier of one sequence: its node count and, per slot (frontier order),
+// the node, its token, the token's hot row (-1: none) and its joint
+// probability -- everything the next expansion and selection need, in one
+// load (no chain through the node arrays and the hot map).
+struct TbSlot {
+    int node, tok, h, pad;
+    double joint;
+};
+struct TbFrontier {
+    int count, pad[3];
+    TbSlot slot[kTbMaxK];
+};
+
+// Hot row of token t (-1 when it has none).
+__device__ __forceinline__ int hot_row(const int32_t *hot_index, int t, int V, int H) {
+    int h = (H > 0 && t >= 0 && t < V) ? hot_index[t] : -1;
+    return h >= H ? -1 : h;
+}
+
 __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
     return a > b ? a : b;
 }
@@ -273,7 +292,7 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
     const int32_t *__restrict__ accept_len, int r, int S, int V, int H, int k, int seg_len,
     TbPart *__restrict__ rows, float *__restrict__ hot_logits, int max_nodes,
     int32_t *__restrict__ node_tok, int32_t *__restrict__ node_par,
-    double *__restrict__ node_joint, int32_t *__restrict__ frontier) {
+    double *__restrict__ node_joint, TbFrontier *__restrict__ frontier) {
     __shared__ double s_exp2[32];
     fill_exp2_table(s_exp2);
     __syncthreads();
@@ -332,8 +351,10 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
         node_tok[(size_t)b * max_nodes] = root_token[b];
         node_par[(size_t)b * max_nodes] = -1;
         node_joint[(size_t)b * max_nodes] = 1.0;
-        frontier[b * (kTbMaxK + 1)] = tb_window(accept_len, b, S, r).count > 0 ? 1 : 0;  // count, ids
-        frontier[b * (kTbMaxK + 1) + 1] = 0;
+        const int t = root_token[b];
+        TbFrontier *fr = frontier + b;
+        fr->count = tb_window(accept_len, b, S, r).count > 0 ? 1 : 0;
+        fr->slot[0] = TbSlot{0, t, hot_row(hot_index, t, V, H), 0, 1.0};
     }
 }
 
@@ -341,22 +362,20 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
 // columns per workgroup: x = l_i[hot[c]] + table[row of the node's token][c].
 __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
     const float *__restrict__ hot_logits, const uint16_t *__restrict__ table,
-    const int32_t *__restrict__ hot_vocab, const int32_t *__restrict__ hot_index,
-    const int32_t *__restrict__ accept_len, int r, int S, int V, int H, int k, int step,
-    int chunk_len, const int32_t *__restrict__ node_tok, int max_nodes,
-    const int32_t *__restrict__ frontier, TbPart *__restrict__ parts) {
+    const int32_t *__restrict__ hot_vocab, const int32_t *__restrict__ accept_len, int r, int S,
+    int V, int H, int k, int step, int chunk_len, const TbFrontier *__restrict__ frontier,
+    TbPart *__restrict__ parts) {
     const int b = blockIdx.x, j = blockIdx.y, c = blockIdx.z;
-    const int *fr = frontier + b * (kTbMaxK + 1);
+    const TbFrontier *fr = frontier + b;
     TbPart *out = parts + ((size_t)b * k + j) * gridDim.z + c;
+    const int count = fr->count;
+    const int h = fr->slot[j].h;                   // loaded with the count (j < kTbMaxK)
     const TbWindow win = tb_window(accept_len, b, S, r);
     if (step >= win.count) return;                 // this sequence's tree is complete
-    if (j >= fr[0]) return;                        // no such frontier node at this step
+    if (j >= count) return;                        // no such frontier node at this step
     __shared__ double s_exp2[32];
     fill_exp2_table(s_exp2);
     __syncthreads();
-    const int t = node_tok[(size_t)b * max_nodes + fr[1 + j]];
-    int h = (t >= 0 && t < V) ? hot_index[t] : -1;
-    if (h >= H) h = -1;
     const float *lh = hot_logits + ((size_t)b * S + win.first + step) * H;
     const uint16_t *trow = table + (size_t)max(h, 0) * H;   // row 0 stands in when h < 0 (unused)
     const int c0 = c * chunk_len, c1 = min(H, c0 + chunk_len);
@@ -393,18 +412,19 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
 // the next frontier.
 __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
     const TbPart *__restrict__ rows, int segs, const TbPart *__restrict__ parts, int chunks,
-    const int32_t *__restrict__ accept_len, int r, int S, int k, int step, int max_nodes,
-    int32_t *__restrict__ node_tok,
+    const int32_t *__restrict__ accept_len, const int32_t *__restrict__ hot_index, int r, int S,
+    int V, int H, int k, int step, int max_nodes, int32_t *__restrict__ node_tok,
     int32_t *__restrict__ node_par, double *__restrict__ node_joint,
-    int32_t *__restrict__ frontier) {
+    TbFrontier *__restrict__ frontier) {
     constexpr int kCandPerLane = 16;          // (segs + chunks) * k <= 64 * 16 candidates
     __shared__ double s_joint[kTbMaxK * kTbMaxK];
+    __shared__ int s_tok[kTbMaxK * kTbMaxK];
     const int b = blockIdx.x;
     const int lane = threadIdx.x & (kWave - 1), j = threadIdx.x / kWave;
     const TbWindow win = tb_window(accept_len, b, S, r);
     if (step >= win.count) return;                 // uniform: this sequence is done
-    int *fr = frontier + b * (kTbMaxK + 1);
-    const int nf = fr[0];
+    TbFrontier *fr = frontier + b;
+    const int nf = fr->count;
     // nodes before this step: the root, then k children per frontier node of
     // every earlier step (1 at step 0, k afterwards)
     const int base = step == 0 ? 1 : 1 + k + (step - 1) * k * k;
@@ -413,7 +433,8 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
         const TbPart *cp = parts + ((size_t)b * k + j) * chunks;
         const int nparts = segs + chunks;
         const int ncand = nparts * k;
-        const int f = fr[1 + j];
+        const TbSlot sl = fr->slot[j];
+        const int f = sl.node;
         // every load of this node is issued before any is used
         float pm = -__builtin_huge_valf();
         double ps = 0.0;
@@ -433,7 +454,7 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
             }
             cand[u] = key;
         }
-        const double pj = node_joint[(size_t)b * max_nodes + f];
+        const double pj = sl.joint;
         float m = pm;
         #pragma unroll
         for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
@@ -459,6 +480,7 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
                 node_par[at] = f;
                 node_joint[at] = joint;
                 s_joint[j * k + r] = joint;
+                s_tok[j * k + r] = tok;
             }
         }
     }
@@ -474,9 +496,12 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
             const double jq = s_joint[q];
             rank += (jq > ji || (jq == ji && q < i)) ? 1 : 0;
         }
-        if (rank < k) fr[1 + rank] = base + i;
+        if (rank < k) {
+            const int t = s_tok[i];
+            fr->slot[rank] = TbSlot{base + i, t, hot_row(hot_index, t, V, H), 0, ji};
+        }
     }
-    if (threadIdx.x == 0) fr[0] = min(k, nc);
+    if (threadIdx.x == 0) fr->count = min(k, nc);
 }
 
 // One workgroup per sequence: keep the `budget` nodes of largest joint
@@ -592,7 +617,7 @@ TreeBuildPlan tree_build_plan(int B, int S, int V, int H, int k) {
     pl.hot_logits_bytes = (size_t)rows * H * sizeof(float);
     pl.parts_bytes = (size_t)B * k * (chunks > 0 ? chunks : 1) * sizeof(TbPart);
     pl.nodes_bytes = (size_t)B * pl.max_nodes * (2 * sizeof(int32_t) + sizeof(double));
-    pl.frontier_bytes = (size_t)B * (kTbMaxK + 1) * sizeof(int32_t);
+    pl.frontier_bytes = (size_t)B * sizeof(TbFrontier);
     return pl;
 }
 
@@ -617,7 +642,7 @@ hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
     int32_t *node_tok = reinterpret_cast<int32_t *>(carve(nn * sizeof(int32_t)));
     int32_t *node_par = reinterpret_cast<int32_t *>(carve(nn * sizeof(int32_t)));
     double *node_joint = reinterpret_cast<double *>(carve(nn * sizeof(double)));
-    int32_t *frontier = reinterpret_cast<int32_t *>(carve(pl.frontier_bytes));
+    TbFrontier *frontier = reinterpret_cast<TbFrontier *>(carve(pl.frontier_bytes));
 
     hipError_t e = launch_kernel(tb_rows_kernel, dim3(B * S, pl.segs), dim3(kTbThreads), s, logits,
                                  hot_vocab, hot_index, root_token, accept_len, r, S, V, H, k,
@@ -626,12 +651,12 @@ hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
     for (int i = 0; i < S && e == hipSuccess; ++i) {
         if (pl.chunks > 0)
             e = launch_kernel(tb_expand_kernel, dim3(B, k, pl.chunks), dim3(kTbThreads), s,
-                              hot_logits, table, hot_vocab, hot_index, accept_len, r, S, V, H, k,
-                              i, pl.chunk_len, node_tok, pl.max_nodes, frontier, parts);
+                              hot_logits, table, hot_vocab, accept_len, r, S, V, H, k, i,
+                              pl.chunk_len, (const TbFrontier *)frontier, parts);
         if (e == hipSuccess)
             e = launch_kernel(tb_select_kernel, dim3(B), dim3(kTbMaxK * kWave), s, rows, pl.segs,
-                              parts, pl.chunks, accept_len, r, S, k, i, pl.max_nodes, node_tok,
-                              node_par, node_joint, frontier);
+                              parts, pl.chunks, accept_len, hot_index, r, S, V, H, k, i,
+                              pl.max_nodes, node_tok, node_par, node_joint, frontier);
     }
     if (e == hipSuccess)
         e = launch_kernel(tb_prune_kernel, dim3(B), dim3(kPruneThreads), s, accept_len, r, S, k,
