@@ -71,16 +71,19 @@ __device__ __forceinline__ int key_index(unsigned long long key) {
     return (int)(0xFFFFFFFFu - (unsigned int)key);
 }
 
+__device__ __forceinline__ double exp_nonpos(double x, const double *tab);
+
 // Running (max, sum of exp(x - max)) of one thread, fp64 sums; a batch of
-// values is folded in with one rescale, without per-value branches.
+// values is folded in with one rescale, without per-value branches. tab: the
+// 2^(j/32) table of exp_nonpos.
 struct OnlineSum {
     float m = -__builtin_huge_valf();
     double s = 0.0;
-    __device__ __forceinline__ void merge(float m2, double s2) {
+    __device__ __forceinline__ void merge(float m2, double s2, const double *tab) {
         if (m2 == -__builtin_huge_valf()) return;
         if (m == -__builtin_huge_valf()) { m = m2; s = s2; return; }
         const float mn = fmaxf(m, m2);
-        s = s * exp((double)m - (double)mn) + s2 * exp((double)m2 - (double)mn);
+        s = s * exp_nonpos((double)m - (double)mn, tab) + s2 * exp_nonpos((double)m2 - (double)mn, tab);
         m = mn;
     }
 };
@@ -209,7 +212,7 @@ __device__ __forceinline__ void fold_chunk(const float (&x)[U], Id id, int k, in
         double sum = 0.0;
         #pragma unroll
         for (int u = 0; u < U; ++u) sum += exp_nonpos((double)x[u] - (double)m, tab);
-        os.merge(m, sum);
+        os.merge(m, sum, tab);
     }
     // k-th largest lane maximum (ties may remove two lanes in one round: the
     // floor only gets lower, never wrong); once the wave's list is full, its
@@ -232,17 +235,22 @@ __device__ __forceinline__ void fold_chunk(const float (&x)[U], Id id, int k, in
 
 // Workgroup reduction of every thread's OnlineSum and every wave's top-k list
 // into one TbPart.
-__device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPart *out) {
+__device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPart *out,
+                                  const double *tab) {
     __shared__ float s_m[kTbWaves];
     __shared__ double s_s[kTbWaves];
     __shared__ unsigned long long s_key[kTbWaves * kTbMaxK];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    // the wave's maximum first, then each lane's sum rescaled to it once and
+    // the sums added (one exponential per lane instead of one per merge)
+    float wm = os.m;
     #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const float m2 = __shfl_xor(os.m, off);
-        const double s2 = __shfl_xor(os.s, off);
-        os.merge(m2, s2);
-    }
+    for (int off = 32; off > 0; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off));
+    double ws = os.m == -__builtin_huge_valf() ? 0.0 : os.s * exp_nonpos((double)os.m - (double)wm, tab);
+    #pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ws += __shfl_xor(ws, off);
+    os.m = wm;
+    os.s = ws;
     if (lane == 0) { s_m[wave] = os.m; s_s[wave] = os.s; }
     if (lane < kTbMaxK) s_key[wave * kTbMaxK + lane] = lane < k ? tk.w : 0ull;
     __syncthreads();
@@ -257,7 +265,7 @@ __device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPar
         if (lane == 0) {
             for (int r = k; r < kTbMaxK; ++r) out->key[r] = 0ull;
             OnlineSum t;
-            for (int w = 0; w < kTbWaves; ++w) t.merge(s_m[w], s_s[w]);
+            for (int w = 0; w < kTbWaves; ++w) t.merge(s_m[w], s_s[w], tab);
             out->m = t.m;
             out->pad = 0;
             out->s = t.s;
@@ -324,7 +332,7 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
         }
         fold_chunk(xv, [&](int u) { return vb + u * kTbThreads; }, k, lane, s_exp2, os, tk);
     }
-    block_reduce_part(os, tk, k, rows + (size_t)row * gridDim.y + seg);
+    block_reduce_part(os, tk, k, rows + (size_t)row * gridDim.y + seg, s_exp2);
     // this row's logits of the hot tokens, contiguous for the per-node passes
     if (H > 0) {
         const int c_len = (H + gridDim.y - 1) / gridDim.y;
@@ -403,7 +411,7 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
         }
         fold_chunk(xv, [&](int u) { return vv[u]; }, k, lane, s_exp2, os, tk);
     }
-    block_reduce_part(os, tk, k, out);
+    block_reduce_part(os, tk, k, out, s_exp2);
 }
 
 // One workgroup per sequence, one wave per frontier node of step i: combine the
@@ -461,6 +469,9 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
         double s = pm == -__builtin_huge_valf() ? 0.0 : ps * exp((double)pm - (double)m);
         #pragma unroll
         for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+        // rank r's key goes to lane r; the children's probabilities are then
+        // computed by lanes 0..k-1 at once
+        unsigned long long mine = 0ull;
         for (int r = 0; r < k; ++r) {
             unsigned long long best = 0ull;
             #pragma unroll
@@ -468,20 +479,21 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
             best = wave_max64(best);
             #pragma unroll
             for (int u = 0; u < kCandPerLane; ++u) cand[u] = cand[u] == best ? 0ull : cand[u];
-            if (lane == 0) {
-                const size_t at = (size_t)b * max_nodes + base + j * k + r;
-                double joint = 0.0;
-                int tok = -1;
-                if (best != 0ull) {
-                    tok = key_index(best);
-                    joint = pj * (exp((double)key_value(best) - (double)m) / s);
-                }
-                node_tok[at] = tok;
-                node_par[at] = f;
-                node_joint[at] = joint;
-                s_joint[j * k + r] = joint;
-                s_tok[j * k + r] = tok;
+            mine = lane == r ? best : mine;
+        }
+        if (lane < k) {
+            const size_t at = (size_t)b * max_nodes + base + j * k + lane;
+            double joint = 0.0;
+            int tok = -1;
+            if (mine != 0ull) {
+                tok = key_index(mine);
+                joint = pj * (exp((double)key_value(mine) - (double)m) / s);
             }
+            node_tok[at] = tok;
+            node_par[at] = f;
+            node_joint[at] = joint;
+            s_joint[j * k + lane] = joint;
+            s_tok[j * k + lane] = tok;
         }
     }
     __syncthreads();
