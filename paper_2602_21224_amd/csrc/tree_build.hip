@@ -418,13 +418,14 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
 // step's row partials with the node's column partials (all loaded at once)
 // into its k children (token, probability, joint probability), then choose
 // the next frontier.
+template <int CPL>          // candidate keys per lane: (segs + chunks) * k <= 64 * CPL
 __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
     const TbPart *__restrict__ rows, int segs, const TbPart *__restrict__ parts, int chunks,
     const int32_t *__restrict__ accept_len, const int32_t *__restrict__ hot_index, int r, int S,
     int V, int H, int k, int step, int max_nodes, int32_t *__restrict__ node_tok,
     int32_t *__restrict__ node_par, double *__restrict__ node_joint,
     TbFrontier *__restrict__ frontier) {
-    constexpr int kCandPerLane = 16;          // (segs + chunks) * k <= 64 * 16 candidates
+    constexpr int kCandPerLane = CPL;
     __shared__ double s_joint[kTbMaxK * kTbMaxK];
     __shared__ int s_tok[kTbMaxK * kTbMaxK];
     const int b = blockIdx.x;
@@ -665,10 +666,16 @@ hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
             e = launch_kernel(tb_expand_kernel, dim3(B, k, pl.chunks), dim3(kTbThreads), s,
                               hot_logits, table, hot_vocab, accept_len, r, S, V, H, k, i,
                               pl.chunk_len, (const TbFrontier *)frontier, parts);
-        if (e == hipSuccess)
-            e = launch_kernel(tb_select_kernel, dim3(B), dim3(kTbMaxK * kWave), s, rows, pl.segs,
-                              parts, pl.chunks, accept_len, hot_index, r, S, V, H, k, i,
-                              pl.max_nodes, node_tok, node_par, node_joint, frontier);
+        if (e == hipSuccess) {
+            // candidate keys per lane of the selection: (segs + chunks) k of them
+            const int ncand = (pl.segs + pl.chunks) * k;
+            auto sel = ncand <= 2 * kWave ? tb_select_kernel<2>
+                       : ncand <= 4 * kWave ? tb_select_kernel<4>
+                       : ncand <= 8 * kWave ? tb_select_kernel<8> : tb_select_kernel<16>;
+            e = launch_kernel(sel, dim3(B), dim3(kTbMaxK * kWave), s, rows, pl.segs, parts,
+                              pl.chunks, accept_len, hot_index, r, S, V, H, k, i, pl.max_nodes,
+                              node_tok, node_par, node_joint, frontier);
+        }
     }
     if (e == hipSuccess)
         e = launch_kernel(tb_prune_kernel, dim3(B), dim3(kPruneThreads), s, accept_len, r, S, k,
