@@ -26,6 +26,7 @@ namespace {
 
 constexpr int kTbThreads = 256;
 constexpr int kTbChunk = 32;               // candidates per thread held in registers at once
+constexpr int kExpThreads = kWave;         // one wave per expansion workgroup: no block reduction
 constexpr int kTbWaves = kTbThreads / kWave;
 constexpr int kPruneThreads = 1024;
 constexpr int kPruneSlots = 4096;          // >= 1 + k + (S - 1) k^2 for k, S <= 16
@@ -273,6 +274,21 @@ __device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPar
     }
 }
 
+// One wave's OnlineSum and top-k list into one TbPart (the wave maximum first,
+// then each lane's sum rescaled to it once; the list is already in lanes
+// 0..k-1).
+__device__ __forceinline__ void wave_reduce_part(const OnlineSum &os, const WaveTopK &tk, int k,
+                                                 int lane, TbPart *out, const double *tab) {
+    float wm = os.m;
+    #pragma unroll
+    for (int off = 32; off > 0; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off));
+    double ws = os.m == -__builtin_huge_valf() ? 0.0 : os.s * exp_nonpos((double)os.m - (double)wm, tab);
+    #pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ws += __shfl_xor(ws, off);
+    if (lane == 0) { out->m = wm; out->pad = 0; out->s = ws; }
+    if (lane < kTbMaxK) out->key[lane] = lane < k ? tk.w : 0ull;
+}
+
 // Steps of sequence b: logits rows [first, first + count). A first tree uses all
 // S rows. A re-sampled tree (Alg. 2; accept_len given) starts after the first
 // rejected position -- the accepted path counts the root, so that position is
@@ -368,7 +384,7 @@ __global__ __launch_bounds__(kTbThreads) void tb_rows_kernel(
 
 // Hot columns of step i for frontier slot j of sequence b, one chunk of the
 // columns per workgroup: x = l_i[hot[c]] + table[row of the node's token][c].
-__global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
+__global__ __launch_bounds__(kExpThreads) void tb_expand_kernel(
     const float *__restrict__ hot_logits, const uint16_t *__restrict__ table,
     const int32_t *__restrict__ hot_vocab, const int32_t *__restrict__ accept_len, int r, int S,
     int V, int H, int k, int step, int chunk_len, const TbFrontier *__restrict__ frontier,
@@ -390,15 +406,15 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
     OnlineSum os;
     WaveTopK tk;
     const int lane = threadIdx.x & (kWave - 1);
-    const int iters = (max(c1 - c0, 0) + kTbThreads - 1) / kTbThreads;   // chunks as above
+    const int iters = (max(c1 - c0, 0) + kExpThreads - 1) / kExpThreads;   // chunks as above
     for (int it0 = 0; it0 < iters; it0 += kTbChunk) {
-        const int cb = c0 + it0 * kTbThreads + (int)threadIdx.x;
+        const int cb = c0 + it0 * kExpThreads + (int)threadIdx.x;
         int vv[kTbChunk];
         float xv[kTbChunk];
         unsigned int rv[kTbChunk];
         #pragma unroll
         for (int u = 0; u < kTbChunk; ++u) {
-            const int cc = min(cb + u * kTbThreads, c1 - 1);
+            const int cc = min(cb + u * kExpThreads, c1 - 1);
             vv[u] = hot_vocab[cc];
             xv[u] = lh[cc];
             rv[u] = trow[cc];
@@ -406,12 +422,12 @@ __global__ __launch_bounds__(kTbThreads) void tb_expand_kernel(
         #pragma unroll
         for (int u = 0; u < kTbChunk; ++u) {
             if (h >= 0) xv[u] += __uint_as_float(rv[u] << 16);
-            const bool use = cb + u * kTbThreads < c1 && vv[u] >= 0 && vv[u] < V;
+            const bool use = cb + u * kExpThreads < c1 && vv[u] >= 0 && vv[u] < V;
             xv[u] = use ? xv[u] : -__builtin_huge_valf();
         }
         fold_chunk(xv, [&](int u) { return vv[u]; }, k, lane, s_exp2, os, tk);
     }
-    block_reduce_part(os, tk, k, out, s_exp2);
+    wave_reduce_part(os, tk, k, lane, out, s_exp2);
 }
 
 // One workgroup per sequence, one wave per frontier node of step i: combine the
@@ -619,7 +635,7 @@ TreeBuildPlan tree_build_plan(int B, int S, int V, int H, int k) {
     pl.seg_len = (int)(((long)V + segs - 1) / segs);
     long chunks = 0;
     if (H > 0) {
-        chunks = ((long)H + 8191) / 8192;            // at least 8192 columns per workgroup
+        chunks = ((long)H + 2047) / 2048;            // at least 2048 columns per (one-wave) workgroup
         if (chunks > 32) chunks = 32;
         if (chunks < 1) chunks = 1;
     }
@@ -663,7 +679,7 @@ hipError_t launch_tree_build(const float *logits, const int32_t *root_token,
                                  node_joint, frontier);
     for (int i = 0; i < S && e == hipSuccess; ++i) {
         if (pl.chunks > 0)
-            e = launch_kernel(tb_expand_kernel, dim3(B, k, pl.chunks), dim3(kTbThreads), s,
+            e = launch_kernel(tb_expand_kernel, dim3(B, k, pl.chunks), dim3(kExpThreads), s,
                               hot_logits, table, hot_vocab, accept_len, r, S, V, H, k, i,
                               pl.chunk_len, (const TbFrontier *)frontier, parts);
         if (e == hipSuccess) {
