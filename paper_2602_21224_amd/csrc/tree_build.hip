@@ -444,6 +444,7 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
     constexpr int kCandPerLane = CPL;
     __shared__ double s_joint[kTbMaxK * kTbMaxK];
     __shared__ int s_tok[kTbMaxK * kTbMaxK];
+    __shared__ int s_hot[kTbMaxK * kTbMaxK];
     const int b = blockIdx.x;
     const int lane = threadIdx.x & (kWave - 1), j = threadIdx.x / kWave;
     const TbWindow win = tb_window(accept_len, b, S, r);
@@ -511,24 +512,32 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
             node_joint[at] = joint;
             s_joint[j * k + lane] = joint;
             s_tok[j * k + lane] = tok;
+            s_hot[j * k + lane] = hot_row(hot_index, tok, V, H);   // loaded now, used after the ranking
         }
     }
     __syncthreads();
     // next frontier: the k children of this step with the largest joint
     // probabilities, largest first, ties to the earlier child. Child i's rank
     // is the number of children before it in that order.
+    // tpc threads share child i's count (consecutive lanes, nc * tpc <= the
+    // workgroup's threads), then add their parts.
     const int nc = nf * k;
-    for (int i = threadIdx.x; i < nc; i += kTbMaxK * kWave) {
-        const double ji = s_joint[i];
+    int tpc = 16;
+    while (tpc > 1 && nc * tpc > kTbMaxK * kWave) tpc >>= 1;
+    {
+        const int i = threadIdx.x / tpc, part = threadIdx.x % tpc;
         int rank = 0;
-        for (int q = 0; q < nc; ++q) {
-            const double jq = s_joint[q];
-            rank += (jq > ji || (jq == ji && q < i)) ? 1 : 0;
+        double ji = 0.0;
+        if (i < nc) {
+            ji = s_joint[i];
+            for (int q = part; q < nc; q += tpc) {
+                const double jq = s_joint[q];
+                rank += (jq > ji || (jq == ji && q < i)) ? 1 : 0;
+            }
         }
-        if (rank < k) {
-            const int t = s_tok[i];
-            fr->slot[rank] = TbSlot{base + i, t, hot_row(hot_index, t, V, H), 0, ji};
-        }
+        for (int off = 1; off < tpc; off <<= 1) rank += __shfl_xor(rank, off);
+        if (i < nc && part == 0 && rank < k)
+            fr->slot[rank] = TbSlot{base + i, s_tok[i], s_hot[i], 0, ji};
     }
     if (threadIdx.x == 0) fr->count = min(k, nc);
 }
