@@ -136,6 +136,63 @@ __device__ __forceinline__ unsigned int wave_max32(unsigned int v) {
                max((unsigned int)__builtin_amdgcn_readlane((int)v, 47), (unsigned int)__builtin_amdgcn_readlane((int)v, 63)));
 }
 
+// Whole-wave reductions without LDS: butterflies inside each row of 16 lanes
+// by DPP (swap neighbours, swap pairs, mirror each half row, mirror the row:
+// after each step every lane of the group holds the group's result), then
+// across rows by the row-pair and half-wave swaps. Every lane ends with the
+// result.
+template <int C>
+__device__ __forceinline__ unsigned int dpp32(unsigned int v) {
+    return (unsigned int)__builtin_amdgcn_update_dpp((int)v, (int)v, C, 0xF, 0xF, false);
+}
+template <int C>
+__device__ __forceinline__ double dpp64(double v) {
+    const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+    const unsigned int lo = dpp32<C>((unsigned int)b), hi = dpp32<C>((unsigned int)(b >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+__device__ __forceinline__ float wave_allmax(float v) {
+    v = fmaxf(v, __uint_as_float(dpp32<kDppXor1>(__float_as_uint(v))));
+    v = fmaxf(v, __uint_as_float(dpp32<kDppXor2>(__float_as_uint(v))));
+    v = fmaxf(v, __uint_as_float(dpp32<kDppHalfMirror>(__float_as_uint(v))));
+    v = fmaxf(v, __uint_as_float(dpp32<kDppMirror>(__float_as_uint(v))));
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(h[0]), __uint_as_float(h[1]));
+}
+
+__device__ __forceinline__ double wave_allsum(double v) {
+    v += dpp64<kDppXor1>(v);
+    v += dpp64<kDppXor2>(v);
+    v += dpp64<kDppHalfMirror>(v);
+    v += dpp64<kDppMirror>(v);
+    #pragma unroll
+    for (int half = 0; half < 2; ++half) {         // row pairs, then the wave's halves
+        const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+        const unsigned int lo = (unsigned int)b, hi = (unsigned int)(b >> 32);
+        const auto l = half == 0 ? __builtin_amdgcn_permlane16_swap(lo, lo, false, false)
+                                 : __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+        const auto h = half == 0 ? __builtin_amdgcn_permlane16_swap(hi, hi, false, false)
+                                 : __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+        v = __longlong_as_double((long long)(((unsigned long long)h[0] << 32) | l[0])) +
+            __longlong_as_double((long long)(((unsigned long long)h[1] << 32) | l[1]));
+    }
+    return v;
+}
+
+// Sum over aligned groups of n consecutive lanes (n = 1, 2, 4, 8 or 16,
+// wave-uniform); every lane of a group ends with the group's sum.
+__device__ __forceinline__ int group_sum(int v, int n) {
+    if (n >= 2) v += (int)dpp32<kDppXor1>((unsigned int)v);
+    if (n >= 4) v += (int)dpp32<kDppXor2>((unsigned int)v);
+    if (n >= 8) v += (int)dpp32<kDppHalfMirror>((unsigned int)v);
+    if (n >= 16) v += (int)dpp32<kDppMirror>((unsigned int)v);
+    return v;
+}
+
 // A wave's top-k list, distributed over lanes: lane j < k holds the (j+1)-th
 // largest key seen by the wave (0 = empty). The k-th key is the wave's
 // admission threshold, so after the first few batches almost no candidate
@@ -244,12 +301,8 @@ __device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPar
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     // the wave's maximum first, then each lane's sum rescaled to it once and
     // the sums added (one exponential per lane instead of one per merge)
-    float wm = os.m;
-    #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off));
-    double ws = os.m == -__builtin_huge_valf() ? 0.0 : os.s * exp_nonpos((double)os.m - (double)wm, tab);
-    #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) ws += __shfl_xor(ws, off);
+    const float wm = wave_allmax(os.m);
+    const double ws = wave_allsum(os.m == -__builtin_huge_valf() ? 0.0 : os.s * exp_nonpos((double)os.m - (double)wm, tab));
     os.m = wm;
     os.s = ws;
     if (lane == 0) { s_m[wave] = os.m; s_s[wave] = os.s; }
@@ -279,12 +332,8 @@ __device__ void block_reduce_part(OnlineSum os, const WaveTopK &tk, int k, TbPar
 // 0..k-1).
 __device__ __forceinline__ void wave_reduce_part(const OnlineSum &os, const WaveTopK &tk, int k,
                                                  int lane, TbPart *out, const double *tab) {
-    float wm = os.m;
-    #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off));
-    double ws = os.m == -__builtin_huge_valf() ? 0.0 : os.s * exp_nonpos((double)os.m - (double)wm, tab);
-    #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) ws += __shfl_xor(ws, off);
+    const float wm = wave_allmax(os.m);
+    const double ws = wave_allsum(os.m == -__builtin_huge_valf() ? 0.0 : os.s * exp_nonpos((double)os.m - (double)wm, tab));
     if (lane == 0) { out->m = wm; out->pad = 0; out->s = ws; }
     if (lane < kTbMaxK) out->key[lane] = lane < k ? tk.w : 0ull;
 }
@@ -409,23 +458,29 @@ __global__ __launch_bounds__(kExpThreads) void tb_expand_kernel(
     const int iters = (max(c1 - c0, 0) + kExpThreads - 1) / kExpThreads;   // chunks as above
     for (int it0 = 0; it0 < iters; it0 += kTbChunk) {
         const int cb = c0 + it0 * kExpThreads + (int)threadIdx.x;
-        int vv[kTbChunk];
-        float xv[kTbChunk];
-        unsigned int rv[kTbChunk];
-        #pragma unroll
-        for (int u = 0; u < kTbChunk; ++u) {
-            const int cc = min(cb + u * kExpThreads, c1 - 1);
-            vv[u] = hot_vocab[cc];
-            xv[u] = lh[cc];
-            rv[u] = trow[cc];
-        }
-        #pragma unroll
-        for (int u = 0; u < kTbChunk; ++u) {
-            if (h >= 0) xv[u] += __uint_as_float(rv[u] << 16);
-            const bool use = cb + u * kExpThreads < c1 && vv[u] >= 0 && vv[u] < V;
-            xv[u] = use ? xv[u] : -__builtin_huge_valf();
-        }
-        fold_chunk(xv, [&](int u) { return vv[u]; }, k, lane, s_exp2, os, tk);
+        // a full chunk needs no per-candidate range tests (kept out of the
+        // common path: they cost registers and instructions)
+        auto chunk = [&](auto full) {
+            int vv[kTbChunk];
+            float xv[kTbChunk];
+            unsigned int rv[kTbChunk];
+            #pragma unroll
+            for (int u = 0; u < kTbChunk; ++u) {
+                const int cc = full ? cb + u * kExpThreads : min(cb + u * kExpThreads, c1 - 1);
+                vv[u] = hot_vocab[cc];
+                xv[u] = lh[cc];
+                rv[u] = trow[cc];
+            }
+            #pragma unroll
+            for (int u = 0; u < kTbChunk; ++u) {
+                if (h >= 0) xv[u] += __uint_as_float(rv[u] << 16);
+                const bool use = (full || cb + u * kExpThreads < c1) && (unsigned int)vv[u] < (unsigned int)V;
+                xv[u] = use ? xv[u] : -__builtin_huge_valf();
+            }
+            fold_chunk(xv, [&](int u) { return vv[u]; }, k, lane, s_exp2, os, tk);
+        };
+        if (c1 - (c0 + it0 * kExpThreads) >= kTbChunk * kExpThreads) chunk(std::true_type{});
+        else chunk(std::false_type{});
     }
     wave_reduce_part(os, tk, k, lane, out, s_exp2);
 }
@@ -481,12 +536,8 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
             cand[u] = key;
         }
         const double pj = sl.joint;
-        float m = pm;
-        #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-        double s = pm == -__builtin_huge_valf() ? 0.0 : ps * exp((double)pm - (double)m);
-        #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+        const float m = wave_allmax(pm);
+        const double s = wave_allsum(pm == -__builtin_huge_valf() ? 0.0 : ps * exp((double)pm - (double)m));
         // rank r's key goes to lane r; the children's probabilities are then
         // computed by lanes 0..k-1 at once
         unsigned long long mine = 0ull;
@@ -535,7 +586,7 @@ __global__ __launch_bounds__(kTbMaxK * kWave) void tb_select_kernel(
                 rank += (jq > ji || (jq == ji && q < i)) ? 1 : 0;
             }
         }
-        for (int off = 1; off < tpc; off <<= 1) rank += __shfl_xor(rank, off);
+        rank = group_sum(rank, tpc);
         if (i < nc && part == 0 && rank < k)
             fr->slot[rank] = TbSlot{base + i, s_tok[i], s_hot[i], 0, ji};
     }
