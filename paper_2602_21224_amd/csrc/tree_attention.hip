@@ -105,6 +105,16 @@ __device__ __forceinline__ float halves_sum(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
+// The same over lanes l, l ^ 16, l ^ 32 and l ^ 48 (the four 16-lane rows of a
+// 16x16 MFMA tile's column), by the row-pair swap and then the half-wave swap.
+__device__ __forceinline__ float rows_max(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return halves_max(fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1])));
+}
+__device__ __forceinline__ float rows_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return halves_sum(__uint_as_float(r[0]) + __uint_as_float(r[1]));
+}
 
 // LDS objects are separate so the compiler can see that only `g_ring` is a
 // target of the asynchronous tile loads.
@@ -784,8 +794,7 @@ __device__ __forceinline__ void narrow_tile(NarrowState<D> &st, unsigned kbase, 
     float mt = kNegInf;
     #pragma unroll
     for (int kb = 0; kb < 4; ++kb) mt = fmaxf(mt, fmaxf(fmaxf(sb[kb][0], sb[kb][1]), fmaxf(sb[kb][2], sb[kb][3])));
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    mt = rows_max(mt);
     const bool raise = mt * c > st.m_run * c + kRescaleSlack;
     if (__any(raise)) {
         const float m_new = raise ? mt : st.m_run;
@@ -1257,9 +1266,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attention_kernel(AttnParams p
             constexpr int kCh = D / 8;
             float *ow = reinterpret_cast<float *>(g_ring);                 // [NW][16][D]
             float *mlw = ow + NW * 16 * D;                                  // [NW][16][2]
-            float lw = ns.l_run;
-            lw += __shfl_xor(lw, 16);
-            lw += __shfl_xor(lw, 32);
+            const float lw = rows_sum(ns.l_run);
             #pragma unroll
             for (int db = 0; db < D / 16; ++db)
                 *reinterpret_cast<f32x4 *>(ow + ((size_t)wave_u * 16 + (lane & 15)) * D + db * 16 +
