@@ -464,12 +464,31 @@ __global__ __launch_bounds__(kExpThreads) void tb_expand_kernel(
             int vv[kTbChunk];
             float xv[kTbChunk];
             unsigned int rv[kTbChunk];
-            #pragma unroll
-            for (int u = 0; u < kTbChunk; ++u) {
-                const int cc = full ? cb + u * kExpThreads : min(cb + u * kExpThreads, c1 - 1);
-                vv[u] = hot_vocab[cc];
-                xv[u] = lh[cc];
-                rv[u] = trow[cc];
+            if constexpr (full) {
+                // four consecutive columns per lane and load (16-byte loads of
+                // the logits and ids, 8-byte loads of the table entries)
+                const int cq = c0 + it0 * kExpThreads + 4 * lane;
+                #pragma unroll
+                for (int q = 0; q < kTbChunk / 4; ++q) {
+                    const int cc = cq + q * 4 * kExpThreads;
+                    const i32x4 v4 = *reinterpret_cast<const i32x4 *>(hot_vocab + cc);
+                    const f32x4 x4 = *reinterpret_cast<const f32x4 *>(lh + cc);
+                    const u16x4 t4 = *reinterpret_cast<const u16x4 *>(trow + cc);
+                    #pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        vv[4 * q + r] = v4[r];
+                        xv[4 * q + r] = x4[r];
+                        rv[4 * q + r] = t4[r];
+                    }
+                }
+            } else {
+                #pragma unroll
+                for (int u = 0; u < kTbChunk; ++u) {
+                    const int cc = min(cb + u * kExpThreads, c1 - 1);
+                    vv[u] = hot_vocab[cc];
+                    xv[u] = lh[cc];
+                    rv[u] = trow[cc];
+                }
             }
             #pragma unroll
             for (int u = 0; u < kTbChunk; ++u) {
@@ -479,8 +498,13 @@ __global__ __launch_bounds__(kExpThreads) void tb_expand_kernel(
             }
             fold_chunk(xv, [&](int u) { return vv[u]; }, k, lane, s_exp2, os, tk);
         };
-        if (c1 - (c0 + it0 * kExpThreads) >= kTbChunk * kExpThreads) chunk(std::true_type{});
-        else chunk(std::false_type{});
+        // full: every column of the chunk exists, and rows, chunk start and the
+        // caller's arrays are aligned for the wide loads
+        if (c1 - (c0 + it0 * kExpThreads) >= kTbChunk * kExpThreads && (H & 3) == 0 && (c0 & 3) == 0 &&
+            (reinterpret_cast<uintptr_t>(hot_vocab) & 15) == 0 && (reinterpret_cast<uintptr_t>(table) & 7) == 0)
+            chunk(std::true_type{});
+        else
+            chunk(std::false_type{});
     }
     wave_reduce_part(os, tk, k, lane, out, s_exp2);
 }
