@@ -498,10 +498,11 @@ __global__ __launch_bounds__(kExpThreads) void tb_expand_kernel(
             }
             fold_chunk(xv, [&](int u) { return vv[u]; }, k, lane, s_exp2, os, tk);
         };
-        // full: every column of the chunk exists, and rows, chunk start and the
-        // caller's arrays are aligned for the wide loads
+        // full: every column of the chunk exists, and rows, chunk start, the
+        // caller's arrays and the workspace row are aligned for the wide loads
         if (c1 - (c0 + it0 * kExpThreads) >= kTbChunk * kExpThreads && (H & 3) == 0 && (c0 & 3) == 0 &&
-            (reinterpret_cast<uintptr_t>(hot_vocab) & 15) == 0 && (reinterpret_cast<uintptr_t>(table) & 7) == 0)
+            (reinterpret_cast<uintptr_t>(hot_vocab) & 15) == 0 && (reinterpret_cast<uintptr_t>(table) & 7) == 0 &&
+            (reinterpret_cast<uintptr_t>(lh) & 15) == 0)
             chunk(std::true_type{});
         else
             chunk(std::false_type{});

@@ -137,6 +137,34 @@ def test_tree_build_reuses_workspace(oracle_mod):
         np.testing.assert_array_equal(nn.cpu().numpy(), want[3])
 
 
+def test_tree_build_workspace_alignment(oracle_mod):
+    """Full expansion chunks load four columns per lane when the rows are 16-byte
+    aligned; a workspace that is only 8-byte aligned (the documented minimum)
+    takes the narrow loads and builds the same trees."""
+    T = U.require_gpu()
+    x = W.make_tree_build_inputs("align", 23, B=2, S=3, V=5000, H=4096, k=4, budget=30)
+    n = T.tree_build_workspace_size(x.B, x.S, x.V, x.H, x.k)
+    ws = torch.empty(n + 16, dtype=torch.uint8, device="cuda")
+    margins = []
+    want = oracle_mod.tree_build(x.logits, x.root, x.table, x.hot_vocab, x.k, x.budget, margins)
+    assert min(margins) > 1e-9
+    tab = U.dev(x.table.view(np.int16)).view(torch.bfloat16)
+    got = []
+    for off in (0, 8):
+        print(f"case workspace offset {off}", flush=True)
+        par, tok, jnt, nn = T.tree_build(U.dev(x.logits), U.dev(x.root), tab, U.dev(x.hot_vocab),
+                                         U.dev(x.hot_index), k=x.k, budget=x.budget,
+                                         workspace=ws[off:off + n])
+        torch.cuda.synchronize()
+        got.append((par.cpu().numpy(), tok.cpu().numpy(), jnt.cpu().numpy(), nn.cpu().numpy()))
+        np.testing.assert_array_equal(got[-1][3], want[3])
+        np.testing.assert_array_equal(got[-1][1], want[1])
+        np.testing.assert_array_equal(got[-1][0], want[0])
+        np.testing.assert_allclose(got[-1][2], want[2], rtol=1e-6, atol=0)
+    for a, b in zip(got[0][:2] + got[0][3:], got[1][:2] + got[1][3:]):
+        np.testing.assert_array_equal(a, b)
+
+
 # ---------------------------------------------------------------- re-sampling (Alg. 2)
 def run_resample(T, x, bonus, alen, r, budget=None, k=None):
     budget = x.budget if budget is None else budget
