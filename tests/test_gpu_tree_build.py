@@ -138,9 +138,10 @@ def test_tree_build_reuses_workspace(oracle_mod):
 
 
 def test_tree_build_workspace_alignment(oracle_mod):
-    """Full expansion chunks load four columns per lane when the rows are 16-byte
-    aligned; a workspace that is only 8-byte aligned (the documented minimum)
-    takes the narrow loads and builds the same trees."""
+    """Full expansion chunks load four columns per lane when the rows and the
+    caller's arrays are aligned for it; a workspace that is only 8-byte aligned
+    (the documented minimum), or a table and hot-id array one element off, take
+    the narrow loads and build the same trees."""
     T = U.require_gpu()
     x = W.make_tree_build_inputs("align", 23, B=2, S=3, V=5000, H=4096, k=4, budget=30)
     n = T.tree_build_workspace_size(x.B, x.S, x.V, x.H, x.k)
@@ -163,6 +164,21 @@ def test_tree_build_workspace_alignment(oracle_mod):
         np.testing.assert_allclose(got[-1][2], want[2], rtol=1e-6, atol=0)
     for a, b in zip(got[0][:2] + got[0][3:], got[1][:2] + got[1][3:]):
         np.testing.assert_array_equal(a, b)
+    # the caller's table and hot ids off the wide loads' alignment (one element
+    # into a larger buffer): the narrow loads, the same trees
+    print("case table and hot ids one element off", flush=True)
+    tbuf = torch.empty(x.H * x.H + 1, dtype=torch.bfloat16, device="cuda")
+    tbuf[1:].copy_(tab.reshape(-1))
+    vbuf = torch.empty(x.H + 1, dtype=torch.int32, device="cuda")
+    vbuf[1:].copy_(U.dev(x.hot_vocab))
+    par, tok, jnt, nn = T.tree_build(U.dev(x.logits), U.dev(x.root), tbuf[1:].view(x.H, x.H),
+                                     vbuf[1:], U.dev(x.hot_index), k=x.k, budget=x.budget,
+                                     workspace=ws[:n])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(nn.cpu().numpy(), want[3])
+    np.testing.assert_array_equal(tok.cpu().numpy(), want[1])
+    np.testing.assert_array_equal(par.cpu().numpy(), want[0])
+    np.testing.assert_allclose(jnt.cpu().numpy(), want[2], rtol=1e-6, atol=0)
 
 
 # ---------------------------------------------------------------- re-sampling (Alg. 2)
